@@ -1,0 +1,173 @@
+"""Seeded synthetic inputs for the phase-owned MoE layer.
+
+This module only draws inputs: router logits, hidden rows and expert
+weights.  It holds none of the layer's own arithmetic (no top-k, no layout,
+no FFN, no combine), and both the CPU oracle's tests and the GPU path's
+tests and benchmark take their inputs from here.
+
+Recipe (the paper's checkpoints and RL traces are internal, so these stand
+in for them): every tensor is drawn as float32 standard normals times a
+scale, in a fixed order from numpy's PCG64 generator: router weight Wg
+[H, E] (std 1/sqrt(H)), the gate/up matrices W_gu[e] [2I, H] one expert at a
+time, the down matrices W_dn[e] [H, I] one expert at a time (all std
+1/sqrt(H)), then the P hidden rows [T_P, H] and the D hidden rows [T_D, H]
+(std 1).  bf16 workloads round every one of them to bfloat16 (round to
+nearest even) and keep the bit patterns; logits are the float32 rounding of
+the float64 product of the (rounded) hidden rows with Wg, plus a per-expert
+bias for skewed routing.  The logits are an input of the routing call, so
+the oracle and the GPU see the very same float32 values.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Optional
+
+import numpy as np
+
+F32 = "f32"
+BF16 = "bf16"
+
+
+@dataclasses.dataclass(frozen=True)
+class LayerSpec:
+    """Shape of one GPU's share of the layer and of its two phase batches."""
+
+    name: str
+    E: int  # expert pool size
+    e0: int  # first resident expert
+    E_loc: int  # resident experts
+    k: int  # top-k
+    H: int  # hidden size
+    I: int  # FFN intermediate size
+    dtype: str  # "f32" or "bf16"
+    T_P: int  # prefill batch tokens
+    T_D: int  # decode batch tokens
+    zipf_s: Optional[float] = None  # skewed routing exponent (None = uniform-ish)
+
+
+# The named workloads.  Sizes follow the paper's model family at one GPU's
+# share: a tiny fp32 check layer, a mid-size bf16 layer, a DeepSeek-V3-shaped
+# expert share (32 resident of 256 routed experts, top-8, H=7168, I=2048) and
+# the same share under Zipf-skewed routing.
+CONFIGS = {
+    0: LayerSpec("tiny-f32", E=8, e0=0, E_loc=8, k=2, H=256, I=512, dtype=F32, T_P=64, T_D=8),
+    1: LayerSpec("mid-bf16", E=32, e0=0, E_loc=32, k=4, H=2048, I=1024, dtype=BF16, T_P=2048, T_D=64),
+    2: LayerSpec("dsv3-share-bf16", E=256, e0=0, E_loc=32, k=8, H=7168, I=2048, dtype=BF16, T_P=8192, T_D=128),
+    3: LayerSpec(
+        "dsv3-share-zipf-bf16", E=256, e0=0, E_loc=32, k=8, H=7168, I=2048, dtype=BF16, T_P=16384, T_D=256, zipf_s=1.2
+    ),
+}
+
+
+def seed_of(cfg: int) -> int:
+    return 1000 + cfg
+
+
+def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round float32 values to bfloat16 (nearest even) and return uint16 bits.
+    Inputs are finite by construction."""
+    a = np.ascontiguousarray(a, np.float32)
+    u = a.view(np.uint32).astype(np.uint64)
+    r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return r.astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """Exact float32 value of bfloat16 bit patterns."""
+    b = np.ascontiguousarray(b, np.uint16)
+    return (b.astype(np.uint32) << 16).view(np.float32)
+
+
+@dataclasses.dataclass
+class LayerInputs:
+    """Everything one GPU's share of the layer consumes.
+
+    Value arrays are float32 (for bf16 workloads they hold exactly the bf16
+    values); `*_bits` hold the bf16 bit patterns the GPU consumes (None for
+    f32 workloads).
+    """
+
+    spec: LayerSpec
+    wg: np.ndarray  # [H, E] f32
+    bias: np.ndarray  # [E] f32 (zeros unless skewed)
+    w_gu: np.ndarray  # [E_loc, 2I, H] f32 values
+    w_dn: np.ndarray  # [E_loc, H, I] f32 values
+    x: dict  # phase -> [T, H] f32 values
+    logits: dict  # phase -> [T, E] f32
+    w_gu_bits: Optional[np.ndarray] = None
+    w_dn_bits: Optional[np.ndarray] = None
+    x_bits: Optional[dict] = None
+
+
+def _draw(rng: np.random.Generator, shape, std: float) -> np.ndarray:
+    a = rng.standard_normal(size=shape, dtype=np.float32)
+    if std != 1.0:
+        a *= np.float32(std)
+    return a
+
+
+def _quant(a: np.ndarray, dtype: str):
+    if dtype == F32:
+        return a, None
+    bits = f32_to_bf16_bits(a)
+    return bf16_bits_to_f32(bits), bits
+
+
+def logits_of(x: np.ndarray, wg: np.ndarray, bias: np.ndarray) -> np.ndarray:
+    """Router logits as float32 rounding of the float64 product, plus bias."""
+    if x.shape[0] == 0:
+        return np.zeros((0, wg.shape[1]), np.float32)
+    l = x.astype(np.float64) @ wg.astype(np.float64)
+    l += bias.astype(np.float64)[None, :]
+    return l.astype(np.float32)
+
+
+def make_layer(spec: LayerSpec, seed: int, bias: Optional[np.ndarray] = None) -> LayerInputs:
+    """Draw one layer's weights and both phase batches in the fixed order."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    H, I, E, E_loc = spec.H, spec.I, spec.E, spec.E_loc
+    wstd = 1.0 / math.sqrt(H)
+    wg = _draw(rng, (H, E), wstd)
+    w_gu = np.empty((E_loc, 2 * I, H), np.float32)
+    for e in range(E_loc):
+        w_gu[e] = _draw(rng, (2 * I, H), wstd)
+    w_dn = np.empty((E_loc, H, I), np.float32)
+    for e in range(E_loc):
+        w_dn[e] = _draw(rng, (H, I), wstd)
+    xs = {0: _draw(rng, (spec.T_P, H), 1.0), 1: _draw(rng, (spec.T_D, H), 1.0)}
+
+    w_gu, w_gu_bits = _quant(w_gu, spec.dtype)
+    w_dn, w_dn_bits = _quant(w_dn, spec.dtype)
+    x, x_bits = {}, {}
+    for ph, a in xs.items():
+        x[ph], x_bits[ph] = _quant(a, spec.dtype)
+    if bias is None:
+        bias = np.zeros(E, np.float32)
+    bias = np.asarray(bias, np.float32)
+    logits = {ph: logits_of(x[ph], wg, bias) for ph in (0, 1)}
+    return LayerInputs(
+        spec=spec,
+        wg=wg,
+        bias=bias,
+        w_gu=w_gu,
+        w_dn=w_dn,
+        x=x,
+        logits=logits,
+        w_gu_bits=w_gu_bits,
+        w_dn_bits=w_dn_bits,
+        x_bits=x_bits if spec.dtype == BF16 else None,
+    )
+
+
+def make_config(cfg: int, seed: Optional[int] = None, bias: Optional[np.ndarray] = None) -> LayerInputs:
+    spec = CONFIGS[cfg]
+    return make_layer(spec, seed_of(cfg) if seed is None else seed, bias=bias)
+
+
+def tie_logits(rng: np.random.Generator, T: int, E: int, levels: int = 4) -> np.ndarray:
+    """Logits drawn from a few discrete levels (with both signed zeros), so
+    that many experts of a token tie; used to exercise tie-breaking."""
+    vals = np.array([-1.5, -0.0, 0.0, 0.75, 2.0, 2.0, 3.25][: max(levels, 3)], np.float32)
+    return rng.choice(vals, size=(T, E)).astype(np.float32)

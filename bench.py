@@ -1,0 +1,304 @@
+#!/usr/bin/env python3
+"""Benchmark: one GPU's share of the phase-owned MoE layer, P and D concurrent.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1]
+
+A step is one pass of the whole layer (route, dispatch, grouped SwiGLU FFN,
+combine) for the prefill batch on one stream and, concurrently, for the
+decode batch on a second stream.  Inputs (weights, hidden rows, logits) are
+seeded synthetic tensors resident in HBM before timing starts.  Prints one
+JSON line with:
+
+* value: whole-job layer throughput, (T_P + T_D) * K / wall time of K steps;
+* d_latency_us: the D layer's GPU latency (events on the D stream) alone and
+  while P layers keep the other stream busy, p50/p90/p99;
+* roofline: the kernel with the largest share of GPU time, its algorithmic
+  bytes or flops per launch over its mean launch duration (HIP events on the
+  stream it runs on, over the timed steps), against the MI355X peak that
+  bounds it;
+* kernels: mean launch duration of every kernel of both phases;
+* cpu_baseline: the CPU oracle timed on a bounded sample on this host.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak, TFLOP/s
+FP32_VECTOR_PEAK_TFLOPS = 157.3
+
+METRIC = "MoE-layer tokens/s (P+D concurrent, 1 GPU); D-layer p50 latency under P load"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=1, help="workload id (0..3); 1 is the headline workload")
+    ap.add_argument("--d-iters", type=int, default=60, help="D layers per latency measurement")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def pct(vals, q):
+    s = sorted(vals)
+    if not s:
+        return None
+    i = min(len(s) - 1, max(0, int(math.ceil(q / 100.0 * len(s))) - 1))
+    return s[i]
+
+
+def workload_name(spec):
+    return (f"{spec.name}: E={spec.E} (resident {spec.E_loc} from e0={spec.e0}) top-{spec.k} H={spec.H} I={spec.I} "
+            f"SwiGLU {spec.dtype}, P {spec.T_P} + D {spec.T_D} tokens concurrent on two streams")
+
+
+def kernel_units(spec, kernel, T, R, touched, esz):
+    """(algorithmic bytes, algorithmic flops) of one launch of `kernel` for a
+    phase batch of T tokens with R resident rows over `touched` experts."""
+    H, I, E, k = spec.H, spec.I, spec.E, spec.k
+    if kernel == "route":
+        return T * E * 4 + T * k * 8, 0
+    if kernel in ("count", "place"):
+        return T * k * 4 * (1 if kernel == "count" else 2) + R * 4, 0
+    if kernel == "permute":
+        tokens_touched = T  # every token row is read once (tokens with no resident slot too)
+        return (tokens_touched + R) * H * esz, 0
+    if kernel == "gemm1_swiglu":
+        return touched * 2 * I * H * esz + R * H * esz + R * I * esz, 4 * R * H * I
+    if kernel == "gemm2_down":
+        return touched * H * I * esz + R * I * esz + R * H * 4, 2 * R * H * I
+    if kernel == "combine":
+        return R * H * 4 + T * H * 4 + T * k * 8, 0
+    return 0, 0
+
+
+def cpu_baseline(inp, seconds):
+    import numpy as np
+
+    import oracle
+
+    spec = inp.spec
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    tokens, reps = 0, 0
+    t0 = time.perf_counter()
+    while True:
+        for ph in (0, 1):
+            oracle.layer(inp.logits[ph], inp.x[ph], inp.w_gu, inp.w_dn, spec.k, spec.e0)
+            tokens += (spec.T_P, spec.T_D)[ph]
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or reps >= 50:
+            break
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        threads = cores
+    del np
+    return {
+        "value": tokens / el,
+        "unit": "tokens/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"{reps} full P ({spec.T_P}) + D ({spec.T_D}) layer passes of the same workload, float64 numpy "
+                  f"oracle, {el:.1f} s",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build runs the path on a single "
+              f"MI355X and has no multi-GPU step.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_00993_amd import moepd as M
+    from synth import BF16, make_config
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    inp = make_config(args.config)
+    spec = inp.spec
+    bf16 = spec.dtype == BF16
+    esz = 2 if bf16 else 4
+
+    def up(a):
+        a = np.ascontiguousarray(a)
+        return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to(dev)
+
+    w_gu = up(inp.w_gu_bits if bf16 else inp.w_gu)
+    w_dn = up(inp.w_dn_bits if bf16 else inp.w_dn)
+    xs = {ph: up(inp.x_bits[ph] if bf16 else inp.x[ph]) for ph in (0, 1)}
+    lg = {ph: up(inp.logits[ph]) for ph in (0, 1)}
+    T = {0: spec.T_P, 1: spec.T_D}
+    outs = {ph: torch.empty((T[ph], spec.H), dtype=torch.float32, device=dev) for ph in (0, 1)}
+    cfg = M.make_config(spec.E, spec.e0, spec.E_loc, spec.k, spec.H, spec.I,
+                        M.MOE_DTYPE_BF16 if bf16 else M.MOE_DTYPE_F32, T[0], T[1])
+    st, ctx = M.moe_ctx_create(cfg, w_gu, w_dn)
+    M.check(st, "moe_ctx_create")
+    sP, sD = torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev)
+    streams = {0: sP, 1: sD}
+
+    def layer(ph):
+        M.layer(ctx, ph, lg[ph], T[ph], xs[ph], outs[ph], streams[ph])
+
+    # ---- warmup
+    for _ in range(max(1, args.warmup)):
+        layer(0)
+        layer(1)
+    torch.cuda.synchronize()
+
+    # ---- timed concurrent steps (per-kernel HIP events on the launching streams)
+    M.check(M.moe_timing_enable(ctx, args.steps), "moe_timing_enable")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        layer(0)
+        layer(1)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern = {}
+    for ph in (0, 1):
+        for kid in range(M.MOE_NUM_KERNELS):
+            st, ms, n = M.moe_timing_read(ctx, ph, kid)
+            M.check(st)
+            if n:
+                kern[(ph, M.moe_kernel_name(kid))] = (ms, n)
+    M.check(M.moe_timing_enable(ctx, 0))
+
+    # rows and touched experts of each phase (device-side layout, read once)
+    rows, touched = {}, {}
+    for ph in (0, 1):
+        st, v = M.moe_phase_view(ctx, ph)
+        M.check(st)
+        counts = torch.empty(spec.E_loc, dtype=torch.int32)
+        import ctypes
+
+        hip = ctypes.CDLL("libamdhip64.so")
+        hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+        assert hip.hipMemcpy(counts.data_ptr(), v.counts, spec.E_loc * 4, 2) == 0
+        rows[ph] = int(counts.sum())
+        touched[ph] = int((counts > 0).sum())
+
+    # ---- D latency alone and under P
+    def d_latencies(under_p):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in
+               range(args.d_iters)]
+        p_first = torch.cuda.Event(enable_timing=True)
+        p_last = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        if under_p:
+            p_first.record(sP)
+            n_p = 4
+            for _ in range(n_p):
+                layer(0)
+        lat = []
+        for i in range(args.d_iters):
+            a, b = evs[i]
+            if under_p:
+                layer(0)  # keep the P stream one layer ahead
+            a.record(sD)
+            layer(1)
+            b.record(sD)
+            if not under_p:
+                sD.synchronize()
+        if under_p:
+            p_last.record(sP)
+        torch.cuda.synchronize()
+        lat = [a.elapsed_time(b) * 1000.0 for a, b in evs]
+        overlapped = None
+        if under_p:
+            overlapped = sum(1 for a, b in evs if p_first.elapsed_time(a) >= 0 and b.elapsed_time(p_last) >= 0)
+        return lat, overlapped
+
+    lat_alone, _ = d_latencies(False)
+    lat_under, overlapped = d_latencies(True)
+
+    # ---- roofline of the dominant kernel
+    tot = {}
+    for (ph, name), (ms, n) in kern.items():
+        tot[(ph, name)] = ms
+    dom = max(tot, key=tot.get)
+    ph_d, name_d = dom
+    ms_d, n_d = kern[dom]
+    avg_s = ms_d / n_d / 1e3
+    by, fl = kernel_units(spec, name_d, T[ph_d], rows[ph_d], touched[ph_d], esz)
+    t_hbm = by / (HBM_PEAK_GBS * 1e9)
+    t_mfma = fl / (MFMA_BF16_PEAK_TFLOPS * 1e12) if bf16 else fl / (FP32_VECTOR_PEAK_TFLOPS * 1e12)
+    if fl and t_mfma >= t_hbm:
+        achieved = fl / avg_s / 1e12
+        peak = MFMA_BF16_PEAK_TFLOPS if bf16 else FP32_VECTOR_PEAK_TFLOPS
+        roof = {"bound": "mfma" if bf16 else "alu", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s"}
+    else:
+        achieved = by / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = round(achieved / roof["peak"], 4)
+    roof["traffic"] = None
+    roof["kernel"] = f"{name_d} ({'P' if ph_d == 0 else 'D'})"
+    roof["per_launch"] = {"bytes": by, "flops": fl, "mean_us": round(avg_s * 1e6, 2), "launches": n_d}
+
+    kernels = {}
+    for (ph, name), (ms, n) in sorted(kern.items()):
+        by_k, fl_k = kernel_units(spec, name, T[ph], rows[ph], touched[ph], esz)
+        us = ms / n * 1e3
+        kernels[f"{'P' if ph == 0 else 'D'}.{name}"] = {
+            "mean_us": round(us, 2),
+            "GB/s": round(by_k / (us * 1e-6) / 1e9, 1) if by_k else None,
+            "TFLOP/s": round(fl_k / (us * 1e-6) / 1e12, 1) if fl_k else None,
+        }
+
+    ms_per_step = wall / args.steps * 1e3
+    value = (T[0] + T[1]) * args.steps / wall
+    p50a, p50u = pct(lat_alone, 50), pct(lat_under, 50)
+    res = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": workload_name(spec), "E": spec.E, "E_loc": spec.E_loc, "top_k": spec.k, "H": spec.H,
+                   "I": spec.I, "T_P": spec.T_P, "T_D": spec.T_D, "rows_P": rows[0], "rows_D": rows[1],
+                   "parallelism": "single GPU, P and D on two streams"},
+        "d_latency_us": {
+            "p50_alone": round(p50a, 2), "p90_alone": round(pct(lat_alone, 90), 2),
+            "p50_under_p": round(p50u, 2), "p90_under_p": round(pct(lat_under, 90), 2),
+            "p99_under_p": round(pct(lat_under, 99), 2), "ratio_p50": round(p50u / p50a, 3),
+            "iters": args.d_iters, "overlapped_with_p": overlapped,
+        },
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    M.check(M.moe_ctx_destroy(ctx))
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,232 @@
+/*
+ * moepd.h -- C ABI of libmoepd: one GPU's share of a DeepEP-style MoE expert
+ * layer, run by a prefill (P) batch and a decode (D) batch concurrently on
+ * shared weights, each phase owning its own mutable state.
+ *
+ * Paper: AInfer-PD, "Communication-Safe In-Place Prefill-Decode Multiplexing
+ * for Distributed MoE Rollouts" (arXiv 2609.00993).
+ *
+ *  - Section 5.1 and its table "Ownership in the concurrent DeepEP runtime":
+ *    P and D share runtime initialisation and model weights but each owns its
+ *    buffers, counters, workspace, stream and events.  Here the context owns
+ *    one such state set per phase; the weights are borrowed and shared.
+ *  - Section 5.1 / Section 6 (first paragraph): phase identity selects state
+ *    explicitly and is never inferred from a host thread or a stream, so every
+ *    call below takes a phase id.  D keeps stable buffer addresses (captured
+ *    graphs replay against them): all phase buffers are allocated once at
+ *    context creation, at capacity.
+ *  - Section 5.2: normal dispatch is split after expert notification, when
+ *    the dispatch shape (per-expert counts) is known and before routed data
+ *    moves.  moe_dispatch runs the notification part (histogram and prefix
+ *    sum, the layout) and then the data movement (token permutation).
+ *  - Section 5.2: at most one pending operation per phase buffer, with
+ *    explicit transitions so that cancellation never reuses partially
+ *    advanced state (the per-phase state machine and moe_phase_reset).
+ *  - Section 5.3: an abandoned operation retires its buffer until a
+ *    quiescent point (moe_phase_reset only succeeds once the phase's last
+ *    enqueued work has completed).
+ *  - Section 4.3 (idle ranks issue matched no-work calls): a batch of
+ *    T = 0 tokens is legal and advances the phase like any other.
+ *
+ * The layer computed (the paper routes tokens to top-k experts, Section 7.1,
+ * but leaves the layer's arithmetic to the engine): softmax over the expert
+ * pool, top-k by logit with ties to the lower expert id (-0.0 == +0.0), the
+ * k weights renormalised; slots routed outside the resident block
+ * [e0, e0 + E_loc) are dropped from this GPU's share; the rows of an expert
+ * are ordered by ascending token; expert e computes
+ * y = (silu(x W1^T) * (x W3^T)) W2^T; out[t] = sum_j w[t,j] y[row(t,j)]
+ * accumulated in float32 in slot order (zero when no slot is resident).
+ * The config dtype is the type of the GEMM operands (x, weights, x_perm, h);
+ * y and out are float32, the accumulation precision, in every context.
+ *
+ * Conventions
+ *  - Every function returns MOE_OK (0) or a negative MOE_ERR_* code.
+ *  - All argument and state validation happens on the host before anything
+ *    is enqueued: a failing call enqueues nothing and changes no state.
+ *  - State transitions happen at enqueue time, not at GPU completion.
+ *  - Device pointers passed in are borrowed: the caller keeps them valid until
+ *    the work enqueued on the given stream has completed.  Output buffers the
+ *    caller passes are written by that work.
+ *  - The library never synchronises a stream, never uses the null stream for
+ *    work and never allocates after moe_ctx_create.  After each call it records
+ *    the phase's event on the stream; if the next call on that phase comes on
+ *    another stream, that stream first waits on the event.
+ *  - One host thread may drive a phase at a time; P and D may be driven from
+ *    different threads, because their host states are disjoint.
+ *  - bf16 data is passed as uint16_t bit patterns (bfloat16), float32 as float.
+ */
+#ifndef MOEPD_H
+#define MOEPD_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOEPD_ABI_VERSION 1
+
+/* Phase ids. */
+enum { MOE_PHASE_P = 0, MOE_PHASE_D = 1, MOE_NUM_PHASES = 2 };
+
+/* Element type of x, the weights, x_perm and h (y and out are always float32). */
+enum { MOE_DTYPE_F32 = 0, MOE_DTYPE_BF16 = 1 };
+
+/* Status codes. */
+enum {
+  MOE_OK = 0,
+  MOE_ERR_INVALID_ARG = -1,   /* bad configuration, null pointer, unsupported size */
+  MOE_ERR_INVALID_PHASE = -2, /* phase id not MOE_PHASE_P or MOE_PHASE_D */
+  MOE_ERR_CAPACITY = -3,      /* T above the phase's max_tokens */
+  MOE_ERR_STATE = -4,         /* call out of order for the phase's state */
+  MOE_ERR_BUSY = -5,          /* phase still has enqueued work in flight */
+  MOE_ERR_OOM = -6,           /* device allocation failed at create */
+  MOE_ERR_HIP = -7            /* a HIP runtime call failed */
+};
+
+/* Per-phase state machine: IDLE -route-> ROUTED -dispatch-> DISPATCHED
+ * -expert_ffn-> COMPUTED -combine-> IDLE. */
+enum { MOE_STATE_IDLE = 0, MOE_STATE_ROUTED = 1, MOE_STATE_DISPATCHED = 2, MOE_STATE_COMPUTED = 3 };
+
+/* Kernels whose launches can be timed (moe_timing_*). */
+enum {
+  MOE_KERNEL_ROUTE = 0,   /* top-k gating */
+  MOE_KERNEL_COUNT = 1,   /* per-chunk expert histogram + prefix sum (dispatch notification) */
+  MOE_KERNEL_PLACE = 2,   /* stable row assignment (dispatch layout) */
+  MOE_KERNEL_PERMUTE = 3, /* token rows -> expert-contiguous rows (dispatch data movement) */
+  MOE_KERNEL_GEMM1 = 4,   /* grouped gate/up GEMM with fused SwiGLU */
+  MOE_KERNEL_GEMM2 = 5,   /* grouped down GEMM */
+  MOE_KERNEL_COMBINE = 6, /* weighted gather-combine */
+  MOE_NUM_KERNELS = 7
+};
+
+typedef struct moe_config {
+  int32_t num_experts;       /* E: routed expert pool, 1..1024 */
+  int32_t expert_begin;      /* e0: first resident expert, >= 0 */
+  int32_t num_local_experts; /* E_loc: resident experts, 1..256, e0 + E_loc <= E */
+  int32_t top_k;             /* k: 1..min(E, 16) */
+  int32_t hidden;            /* H: multiple of 64, 64..16384 */
+  int32_t inter;             /* I: multiple of 64, 64..16384 */
+  int32_t dtype;             /* MOE_DTYPE_F32 or MOE_DTYPE_BF16 */
+  int32_t max_tokens[MOE_NUM_PHASES]; /* capacity per phase, 0..1048576 */
+  int32_t flags;             /* must be 0 */
+} moe_config_t;
+
+/* Borrowed, read-only expert weights for the E_loc resident experts, shared by
+ * both phases (row-major, dtype of the config):
+ *   w_gate_up [E_loc, 2I, H]: rows [0, I) = W1 (gate), rows [I, 2I) = W3 (up)
+ *   w_down    [E_loc, H, I]:  W2
+ * They must stay valid for the context's lifetime. */
+typedef struct moe_weights {
+  const void* w_gate_up;
+  const void* w_down;
+} moe_weights_t;
+
+/* Device pointers and sizes of one phase's owned buffers (read-only for the
+ * caller; contents are those left by the last completed call):
+ *   topk_idx    [T, k] int32  global expert ids, slot j = j-th largest logit
+ *   topk_w      [T, k] float  renormalised gate weights
+ *   counts      [E_loc] int32 rows per resident expert
+ *   offsets     [E_loc+1] int32 exclusive prefix sum of counts
+ *   row_of_slot [T, k] int32  row of slot (t, j) in x_perm, -1 if dropped
+ *   token_of_row[R]    int32  token of each row, R = offsets[E_loc]
+ *   x_perm [R, H], h [R, I] in the config dtype; y [R, H] float32
+ * Capacities: T <= max_tokens[phase], R <= rows_capacity. */
+typedef struct moe_phase_view {
+  int32_t state;
+  int32_t tokens;        /* T of the batch in flight (last routed) */
+  int32_t rows_capacity; /* max_tokens * min(k, E_loc) */
+  int32_t reserved;
+  int32_t* topk_idx;
+  float* topk_w;
+  int32_t* counts;
+  int32_t* offsets;
+  int32_t* row_of_slot;
+  int32_t* token_of_row;
+  void* x_perm;
+  void* h;
+  float* y;
+} moe_phase_view_t;
+
+typedef struct moe_ctx moe_ctx_t;
+
+/* Create a context on the current HIP device.  Validates cfg (see field
+ * comments), allocates both phases' buffers at capacity (disjoint
+ * allocations, fixed for the context's lifetime) and their events.  Creates no
+ * stream.  Errors: MOE_ERR_INVALID_ARG (null pointer, size out of range, k > E,
+ * e0 + E_loc > E, flags != 0), MOE_ERR_OOM, MOE_ERR_HIP.  On error *out is
+ * NULL and nothing is left allocated. */
+int moe_ctx_create(const moe_config_t* cfg, const moe_weights_t* w, moe_ctx_t** out);
+
+/* Top-k gating of T tokens (phase state IDLE -> ROUTED).
+ * logits: borrowed device [T, E] float32, row-major, finite values.
+ * Writes the phase's topk_idx and topk_w.  T = 0 is legal.
+ * Errors: MOE_ERR_INVALID_ARG (null ctx; null logits with T > 0; T < 0),
+ * MOE_ERR_INVALID_PHASE, MOE_ERR_CAPACITY, MOE_ERR_STATE, MOE_ERR_HIP. */
+int moe_route(moe_ctx_t* ctx, int phase, const float* logits, int32_t T, hipStream_t stream);
+
+/* Dispatch (ROUTED -> DISPATCHED): the notification part computes counts,
+ * offsets, row_of_slot and token_of_row (rows of an expert in ascending token
+ * order, no padding); the data part copies x[t] into x_perm[row] for every
+ * resident slot.  x: borrowed device [T, H] in the config dtype (T from the
+ * preceding moe_route).  Errors: MOE_ERR_INVALID_ARG (null x with T > 0),
+ * MOE_ERR_INVALID_PHASE, MOE_ERR_STATE, MOE_ERR_HIP. */
+int moe_dispatch(moe_ctx_t* ctx, int phase, const void* x, hipStream_t stream);
+
+/* Grouped expert FFN (DISPATCHED -> COMPUTED): h = silu(x_perm W1^T) *
+ * (x_perm W3^T) and y = h W2^T for the rows of every resident expert.  bf16
+ * contexts multiply bf16 operands with float32 accumulation, round h to bf16
+ * (nearest even; h is GEMM2's operand) and keep y in float32; float32
+ * contexts compute everything in float32.  The tile schedule
+ * is read from the device-side offsets (no host synchronisation).
+ * Errors: MOE_ERR_INVALID_ARG, MOE_ERR_INVALID_PHASE, MOE_ERR_STATE, MOE_ERR_HIP. */
+int moe_expert_ffn(moe_ctx_t* ctx, int phase, hipStream_t stream);
+
+/* Weighted combine (COMPUTED -> IDLE): out[t] = sum over resident slots j, in
+ * slot order, of topk_w[t,j] * y[row_of_slot[t,j]], accumulated in float32;
+ * tokens with no resident slot get a zero row.
+ * out: borrowed device [T, H] float32; every row is written.
+ * Errors: MOE_ERR_INVALID_ARG (null out with T > 0), MOE_ERR_INVALID_PHASE,
+ * MOE_ERR_STATE, MOE_ERR_HIP. */
+int moe_combine(moe_ctx_t* ctx, int phase, void* out, hipStream_t stream);
+
+/* Fill *view with the phase's buffer pointers and state.
+ * Errors: MOE_ERR_INVALID_ARG (null), MOE_ERR_INVALID_PHASE. */
+int moe_phase_view(const moe_ctx_t* ctx, int phase, moe_phase_view_t* view);
+
+/* Explicit transition back to IDLE (cancellation).  Succeeds only when every
+ * operation enqueued for the phase has completed on the GPU; otherwise returns
+ * MOE_ERR_BUSY and changes nothing.  Never touches the other phase.
+ * Errors: MOE_ERR_INVALID_ARG, MOE_ERR_INVALID_PHASE, MOE_ERR_BUSY, MOE_ERR_HIP. */
+int moe_phase_reset(moe_ctx_t* ctx, int phase);
+
+/* Wait for both phases' enqueued work, then free every buffer and event the
+ * context owns.  Never touches the borrowed weights.  NULL is a no-op. */
+int moe_ctx_destroy(moe_ctx_t* ctx);
+
+/* Static description of a status code (never NULL). */
+const char* moe_status_string(int status);
+
+/* ---- measurement aids ------------------------------------------------------
+ * With timing enabled, every kernel launch of both phases is bracketed by a
+ * pair of HIP events recorded on the stream the kernel is launched on.  Up to
+ * max_launches launches are kept per (phase, kernel); later launches are not
+ * timed.  Enabling allocates the events (call it before timed work);
+ * max_launches = 0 disables timing and frees them.
+ * Errors: MOE_ERR_INVALID_ARG, MOE_ERR_BUSY (work in flight), MOE_ERR_HIP. */
+int moe_timing_enable(moe_ctx_t* ctx, int32_t max_launches);
+
+/* Sum of the recorded launch durations (milliseconds) and their number for
+ * one (phase, kernel), after waiting for the recorded events; then clears the
+ * records.  Errors: MOE_ERR_INVALID_ARG, MOE_ERR_INVALID_PHASE, MOE_ERR_HIP. */
+int moe_timing_read(moe_ctx_t* ctx, int phase, int kernel, double* total_ms, int32_t* launches);
+
+/* Name of a MOE_KERNEL_* id ("?" when out of range). */
+const char* moe_kernel_name(int kernel);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOEPD_H */

@@ -1,0 +1,319 @@
+// Grouped expert FFN in bf16 on CDNA4 matrix cores (fp32 accumulation).
+//
+// GEMM1 (gated): for the rows [offsets[e], offsets[e+1]) of expert e,
+//   h = silu(x_perm W1^T) * (x_perm W3^T), W1/W3 = rows [0,I)/[I,2I) of W_gu[e],
+// with the SwiGLU applied in the epilogue so g and u never reach memory.
+// GEMM2: y = h W2^T with W2 = W_dn[e].  h is rounded to bf16 (nearest even),
+// the operand type of GEMM2; y stays float32, the accumulation precision.  The paper's engine runs its own expert kernels (Section 7.1 states
+// BF16 and FP8 checkpoints); this is a gfx950 design of the same contraction.
+//
+// Scheduling is fully device-side: the dispatch scan leaves tile_base, the
+// prefix sum of m-tiles per expert, and each workgroup finds its tile from
+// its id, so no host synchronisation is needed between dispatch and FFN.  The
+// grid is an upper bound; surplus workgroups exit at once.  Tile ids run
+// expert-major, then n-tile, then m-tile, and consecutive ids stay on one XCD
+// (the dispatcher deals workgroups round-robin to the 8 XCDs): the m-tiles of
+// one expert that share a weight tile run side by side on one XCD's L2.
+//
+// Two tile shapes:
+//  * large batches (prefill): 256 threads, BMxBN output tile, K staged through
+//    LDS in 64-deep double-buffered slices (16-byte chunks, XOR-swizzled rows
+//    so the MFMA fragment reads are bank-conflict free), 32x32x16 MFMAs;
+//  * small batches (decode, a few rows per expert): the layer is a weight
+//    stream, so each wave reads its weight rows straight into MFMA operand
+//    registers (no LDS round trip), one 32-row m-tile and 32 columns per wave,
+//    with the next K slice in flight while the current one is multiplied.
+#include "common.h"
+#include "kernels.h"
+
+namespace moepd {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+struct GemmArgs {
+  const uint16_t* A;       // [R, K] expert-contiguous rows
+  const uint16_t* B;       // expert e at B + e * b_stride, rows of length K
+  void* C;                 // [R, N]: bf16 h (gated) or float32 y
+  const int32_t* offsets;  // [E_loc + 1]
+  const int32_t* tile_base;
+  long long b_stride;
+  int e_loc, N, K, n_tiles, up_row;
+};
+
+struct TileCoord {
+  int e, m0, m_end, n0;
+};
+
+__device__ __forceinline__ bool tile_lookup(const GemmArgs& g, int bm, int bn, TileCoord& tc) {
+  const int total = g.tile_base[g.e_loc] * g.n_tiles;
+  const int per_xcd = (total + 7) >> 3;
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  if (slot >= per_xcd) return false;
+  const int L = xcd * per_xcd + slot;
+  if (L >= total) return false;
+  int lo = 0, hi = g.e_loc - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (g.tile_base[mid] * g.n_tiles <= L) lo = mid;
+    else hi = mid - 1;
+  }
+  const int e = lo;
+  const int mt_e = g.tile_base[e + 1] - g.tile_base[e];
+  const int local = L - g.tile_base[e] * g.n_tiles;
+  const int nt = local / mt_e, mt = local - nt * mt_e;
+  tc.e = e;
+  tc.m0 = g.offsets[e] + mt * bm;
+  tc.m_end = g.offsets[e + 1];
+  tc.n0 = nt * bn;
+  return true;
+}
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(const u32x4& u) { return __builtin_bit_cast(bf16x8_t, u); }
+
+__device__ __forceinline__ float silu_mul(float gt, float up) { return gt / (1.f + __expf(-gt)) * up; }
+
+// Row i of the 32x32 accumulator element r held by `lane` (column = lane & 31).
+__device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
+
+// ------------------------------------------------------------------ tiled (prefill)
+
+template <int BM, int BN, int WM, int WN, bool GATED>
+__global__ __launch_bounds__(WM* WN * 64) void gemm_tiled(GemmArgs g) {
+  constexpr int BK = 64;
+  constexpr int NT = WM * WN * 64;
+  constexpr int NB = GATED ? 2 : 1;
+  constexpr int BR = NB * BN;  // weight rows staged per tile
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int FM = WTM / 32, FN = WTN / 32;
+  constexpr int AC = BM * 8 / NT, BC = BR * 8 / NT;  // 16-byte chunks per thread per slice
+  static_assert(FM * 32 == WTM && FN * 32 == WTN, "wave tile must be a multiple of 32x32");
+  static_assert(AC * NT == BM * 8 && BC * NT == BR * 8, "tile must split evenly over the threads");
+  __shared__ u32x4 As[2][BM * 8];
+  __shared__ u32x4 Bs[2][BR * 8];
+
+  TileCoord tc;
+  if (!tile_lookup(g, BM, BN, tc)) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const uint16_t* Be = g.B + (size_t)tc.e * g.b_stride;
+
+  const u32x4* a_src[AC];
+  int a_dst[AC];
+#pragma unroll
+  for (int i = 0; i < AC; ++i) {
+    const int q = tid + i * NT, r = q >> 3, c = q & 7;
+    const int row = min(tc.m0 + r, tc.m_end - 1);
+    a_src[i] = reinterpret_cast<const u32x4*>(g.A + (size_t)row * g.K) + c;
+    a_dst[i] = r * 8 + (c ^ (r & 7));
+  }
+  const u32x4* b_src[BC];
+  int b_dst[BC];
+#pragma unroll
+  for (int i = 0; i < BC; ++i) {
+    const int q = tid + i * NT, r = q >> 3, c = q & 7;
+    int brow;
+    if (GATED) brow = r < BN ? min(tc.n0 + r, g.N - 1) : g.up_row + min(tc.n0 + r - BN, g.N - 1);
+    else brow = min(tc.n0 + r, g.N - 1);
+    b_src[i] = reinterpret_cast<const u32x4*>(Be + (size_t)brow * g.K) + c;
+    b_dst[i] = r * 8 + (c ^ (r & 7));
+  }
+
+  u32x4 ra[AC], rb[BC];
+  f32x16_t acc[FM][FN * NB];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN * NB; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int KT = g.K / BK;
+#pragma unroll
+  for (int i = 0; i < AC; ++i) ra[i] = a_src[i][0];
+#pragma unroll
+  for (int i = 0; i < BC; ++i) rb[i] = b_src[i][0];
+#pragma unroll
+  for (int i = 0; i < AC; ++i) As[0][a_dst[i]] = ra[i];
+#pragma unroll
+  for (int i = 0; i < BC; ++i) Bs[0][b_dst[i]] = rb[i];
+  __syncthreads();
+
+  for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < KT) {
+#pragma unroll
+      for (int i = 0; i < AC; ++i) ra[i] = a_src[i][(kt + 1) * 8];
+#pragma unroll
+      for (int i = 0; i < BC; ++i) rb[i] = b_src[i][(kt + 1) * 8];
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int ch = 2 * s + (lane >> 5);
+      bf16x8_t af[FM], bfr[FN * NB];
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) {
+        const int r = wm * WTM + fm * 32 + (lane & 31);
+        af[fm] = as_bf16x8(As[cur][r * 8 + (ch ^ (r & 7))]);
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+          const int r = nb * BN + wn * WTN + fn * 32 + (lane & 31);
+          bfr[nb * FN + fn] = as_bf16x8(Bs[cur][r * 8 + (ch ^ (r & 7))]);
+        }
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int j = 0; j < FN * NB; ++j)
+          acc[fm][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[fm], bfr[j], acc[fm][j], 0, 0, 0);
+    }
+    if (kt + 1 < KT) {
+#pragma unroll
+      for (int i = 0; i < AC; ++i) As[cur ^ 1][a_dst[i]] = ra[i];
+#pragma unroll
+      for (int i = 0; i < BC; ++i) Bs[cur ^ 1][b_dst[i]] = rb[i];
+    }
+    __syncthreads();
+  }
+
+  // epilogue
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const int col = tc.n0 + wn * WTN + fn * 32 + (lane & 31);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = tc.m0 + wm * WTM + fm * 32 + acc_row(r, lane);
+        if (row < tc.m_end && col < g.N) {
+          if (GATED)
+            static_cast<uint16_t*>(g.C)[(size_t)row * g.N + col] =
+                f32_to_bf16(silu_mul(acc[fm][fn][r], acc[fm][FN + fn][r]));
+          else
+            static_cast<float*>(g.C)[(size_t)row * g.N + col] = acc[fm][fn][r];
+        }
+      }
+    }
+}
+
+// ------------------------------------------------------------------ skinny (decode)
+
+template <bool GATED>
+__global__ __launch_bounds__(256) void gemm_skinny(GemmArgs g) {
+  constexpr int BM = 32, BN = 128;
+  constexpr int NB = GATED ? 2 : 1;
+  TileCoord tc;
+  if (!tile_lookup(g, BM, BN, tc)) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 31, kg = lane >> 5;
+  const int arow = min(tc.m0 + r, tc.m_end - 1);
+  const int col = tc.n0 + wave * 32 + r;
+  const int colc = min(col, g.N - 1);
+  const uint16_t* Be = g.B + (size_t)tc.e * g.b_stride;
+  // lane group kg holds k in [64*kb + 32*kg, +32) as four 16-byte chunks;
+  // MFMA step s takes chunk s of both groups (the same k map for A and B).
+  const u32x4* pa = reinterpret_cast<const u32x4*>(g.A + (size_t)arow * g.K) + kg * 4;
+  const u32x4* pb[NB];
+  pb[0] = reinterpret_cast<const u32x4*>(Be + (size_t)colc * g.K) + kg * 4;
+  if (GATED) pb[NB - 1] = reinterpret_cast<const u32x4*>(Be + (size_t)(g.up_row + colc) * g.K) + kg * 4;
+
+  f32x16_t acc[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[j][q] = 0.f;
+
+  const int KB = g.K / 64;
+  u32x4 a0[4], b0[NB][4], a1[4], b1[NB][4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    a0[s] = pa[s];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) b0[j][s] = pb[j][s];
+  }
+  for (int kb = 0; kb < KB; ++kb) {
+    if (kb + 1 < KB) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        a1[s] = pa[(kb + 1) * 8 + s];
+#pragma unroll
+        for (int j = 0; j < NB; ++j) b1[j][s] = pb[j][(kb + 1) * 8 + s];
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a0[s]), as_bf16x8(b0[j][s]), acc[j], 0, 0, 0);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      a0[s] = a1[s];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) b0[j][s] = b1[j][s];
+    }
+  }
+
+  if (col < g.N) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int row = tc.m0 + acc_row(q, lane);
+      if (row < tc.m_end) {
+        if (GATED)
+          static_cast<uint16_t*>(g.C)[(size_t)row * g.N + col] = f32_to_bf16(silu_mul(acc[0][q], acc[NB - 1][q]));
+        else
+          static_cast<float*>(g.C)[(size_t)row * g.N + col] = acc[0][q];
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ launch
+
+int ffn_bf16_bm(int regime) { return regime == 0 ? 128 : 32; }
+
+static inline int round8(long long v) { return (int)((v + 7) / 8 * 8); }
+
+hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
+                           int e_loc, int H, int I, int max_m_tiles, hipStream_t s) {
+  GemmArgs g;
+  g.offsets = b.offsets;
+  g.tile_base = b.tile_base;
+  g.e_loc = e_loc;
+  if (gemm == 1) {
+    g.A = (const uint16_t*)b.x_perm;
+    g.B = (const uint16_t*)w_gu;
+    g.C = b.h;
+    g.b_stride = 2LL * I * H;
+    g.N = I;
+    g.K = H;
+    g.up_row = I;
+  } else {
+    g.A = (const uint16_t*)b.h;
+    g.B = (const uint16_t*)w_dn;
+    g.C = b.y;
+    g.b_stride = (long long)H * I;
+    g.N = H;
+    g.K = I;
+    g.up_row = 0;
+  }
+  if (regime == 0) {
+    if (gemm == 1) {
+      g.n_tiles = (g.N + 127) / 128;
+      gemm_tiled<128, 128, 2, 2, true><<<round8((long long)max_m_tiles * g.n_tiles), 256, 0, s>>>(g);
+    } else {
+      g.n_tiles = (g.N + 255) / 256;
+      gemm_tiled<128, 256, 2, 2, false><<<round8((long long)max_m_tiles * g.n_tiles), 256, 0, s>>>(g);
+    }
+  } else {
+    g.n_tiles = (g.N + 127) / 128;
+    if (gemm == 1)
+      gemm_skinny<true><<<round8((long long)max_m_tiles * g.n_tiles), 256, 0, s>>>(g);
+    else
+      gemm_skinny<false><<<round8((long long)max_m_tiles * g.n_tiles), 256, 0, s>>>(g);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace moepd

@@ -1,0 +1,74 @@
+// Internal launch interface between the host runtime (ctx.hip) and the
+// kernels.  Every launcher enqueues on the given stream and returns the
+// hipError_t of the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moepd {
+
+// One phase's device buffers (owned by the context, see moepd.h).
+struct PhaseBuffers {
+  int32_t* topk_idx;      // [Tmax, k]
+  float* topk_w;          // [Tmax, k]
+  int32_t* counts;        // [E_loc]
+  int32_t* offsets;       // [E_loc + 1]
+  int32_t* row_of_slot;   // [Tmax, k]
+  int32_t* token_of_row;  // [Rcap]
+  void* x_perm;           // [Rcap, H]
+  void* h;                // [Rcap, I]
+  float* y;               // [Rcap, H] float32
+  // workspace
+  int32_t* chunk_counts;  // [E_loc * max_chunks], expert-major
+  int32_t* chunk_base;    // [E_loc * max_chunks], first row of (expert, chunk)
+  int32_t* tile_base;     // [E_loc + 1], prefix sum of m-tiles per expert
+  uint32_t* done;         // [1], arrival counter of the count kernel (returns to 0)
+};
+
+// Largest number of (expert, chunk) histogram cells the count kernel scans.
+constexpr int kMaxCells = 8192;
+constexpr int kMaxTopK = 16;
+constexpr int kMaxExperts = 1024;
+constexpr int kMaxLocalExperts = 256;
+
+// Dispatch chunking: tokens per chunk for a batch of T tokens.
+inline int dispatch_chunk_tokens(int T, int k, int e_loc) {
+  int tc = (256 + k - 1) / k;
+  int need = (int)(((long long)T * e_loc + kMaxCells - 1) / kMaxCells);
+  if (need > tc) tc = need;
+  return tc < 1 ? 1 : tc;
+}
+
+hipError_t launch_route(const float* logits, int T, int E, int k, int32_t* topk_idx, float* topk_w,
+                        hipStream_t s);
+
+// Histogram of each chunk's slots per local expert, then (last block) the
+// exclusive scan giving counts, offsets, chunk bases and m-tile prefix.
+hipError_t launch_count(const int32_t* topk_idx, int T, int k, int e0, int e_loc, int chunk_tokens, int nchunks,
+                        int bm, const PhaseBuffers& b, hipStream_t s);
+
+// Stable rows for every slot: row_of_slot and token_of_row.
+hipError_t launch_place(const int32_t* topk_idx, int T, int k, int e0, int e_loc, int chunk_tokens, int nchunks,
+                        const PhaseBuffers& b, hipStream_t s);
+
+// x_perm[row] = x[t] for every resident slot (row-byte granularity 16 B).
+hipError_t launch_permute(const void* x, int T, int k, int row_bytes, const int32_t* row_of_slot, void* x_perm,
+                          hipStream_t s);
+
+// out[t] = sum_j w[t,j] y[row(t,j)] in float32 (y and out are float32).
+hipError_t launch_combine(const void* y, const float* topk_w, const int32_t* row_of_slot, int T, int k, int H,
+                          void* out, hipStream_t s);
+
+// Grouped expert FFN.  `regime` picks the tile configuration (0 = large
+// batches, 1 = small batches); bm_of_regime gives its m-tile height, which
+// the count kernel must use for tile_base.
+int ffn_bf16_bm(int regime);
+hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
+                           int e_loc, int H, int I, int max_m_tiles, hipStream_t s);
+
+int ffn_f32_bm();
+hipError_t launch_ffn_f32(int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn, int e_loc, int H,
+                          int I, int max_m_tiles, hipStream_t s);
+
+}  // namespace moepd

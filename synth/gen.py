@@ -6,12 +6,13 @@ no FFN, no combine), and both the CPU oracle's tests and the GPU path's
 tests and benchmark take their inputs from here.
 
 Recipe (the paper's checkpoints and RL traces are internal, so these stand
-in for them): every tensor is drawn as float32 standard normals times a
-scale, in a fixed order from numpy's PCG64 generator: router weight Wg
-[H, E] (std 1/sqrt(H)), the gate/up matrices W_gu[e] [2I, H] one expert at a
-time, the down matrices W_dn[e] [H, I] one expert at a time (all std
-1/sqrt(H)), then the P hidden rows [T_P, H] and the D hidden rows [T_D, H]
-(std 1).  bf16 workloads round every one of them to bfloat16 (round to
+in for them): every tensor block is drawn as float32 standard normals times a
+scale from its own numpy PCG64 stream, seeded by SeedSequence([seed, id]):
+id 0 is the router weight Wg [H, E] (std 1/sqrt(H)), ids 1..E_loc the
+gate/up matrices W_gu[e] [2I, H], ids E_loc+1..2 E_loc the down matrices
+W_dn[e] [H, I] (all std 1/sqrt(H)), then 2 E_loc+1 the P hidden rows [T_P, H]
+and 2 E_loc+2 the D hidden rows [T_D, H] (std 1).  Separate streams let the
+blocks be drawn in parallel with results independent of the thread count.  bf16 workloads round every one of them to bfloat16 (round to
 nearest even) and keep the bit patterns; logits are the float32 rounding of
 the float64 product of the (rounded) hidden rows with Wg, plus a per-expert
 bias for skewed routing.  The logits are an input of the routing call, so
@@ -20,8 +21,10 @@ the oracle and the GPU see the very same float32 values.
 
 from __future__ import annotations
 
+import concurrent.futures as cf
 import dataclasses
 import math
+import os
 from typing import Optional
 
 import numpy as np
@@ -67,10 +70,9 @@ def seed_of(cfg: int) -> int:
 
 def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
     """Round float32 values to bfloat16 (nearest even) and return uint16 bits.
-    Inputs are finite by construction."""
-    a = np.ascontiguousarray(a, np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    Inputs are finite by construction (no overflow of the 32-bit sum)."""
+    u = np.ascontiguousarray(a, np.float32).view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
     return r.astype(np.uint16)
 
 
@@ -101,18 +103,23 @@ class LayerInputs:
     x_bits: Optional[dict] = None
 
 
-def _draw(rng: np.random.Generator, shape, std: float) -> np.ndarray:
-    a = rng.standard_normal(size=shape, dtype=np.float32)
+def _stream(seed: int, block: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, block])))
+
+
+def _draw_block(seed: int, block: int, shape, std: float, dtype: str):
+    """One tensor block: float32 normals * std, rounded to bf16 if asked.
+    Returns (float32 values, bf16 bits or None)."""
+    a = _stream(seed, block).standard_normal(size=shape, dtype=np.float32)
     if std != 1.0:
         a *= np.float32(std)
-    return a
-
-
-def _quant(a: np.ndarray, dtype: str):
     if dtype == F32:
         return a, None
     bits = f32_to_bf16_bits(a)
     return bf16_bits_to_f32(bits), bits
+
+
+_POOL_WORKERS = max(1, min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else 4))
 
 
 def logits_of(x: np.ndarray, wg: np.ndarray, bias: np.ndarray) -> np.ndarray:
@@ -125,24 +132,37 @@ def logits_of(x: np.ndarray, wg: np.ndarray, bias: np.ndarray) -> np.ndarray:
 
 
 def make_layer(spec: LayerSpec, seed: int, bias: Optional[np.ndarray] = None) -> LayerInputs:
-    """Draw one layer's weights and both phase batches in the fixed order."""
-    rng = np.random.Generator(np.random.PCG64(seed))
+    """Draw one layer's weights and both phase batches (see the module recipe)."""
     H, I, E, E_loc = spec.H, spec.I, spec.E, spec.E_loc
     wstd = 1.0 / math.sqrt(H)
-    wg = _draw(rng, (H, E), wstd)
+    bf16 = spec.dtype == BF16
     w_gu = np.empty((E_loc, 2 * I, H), np.float32)
-    for e in range(E_loc):
-        w_gu[e] = _draw(rng, (2 * I, H), wstd)
     w_dn = np.empty((E_loc, H, I), np.float32)
-    for e in range(E_loc):
-        w_dn[e] = _draw(rng, (H, I), wstd)
-    xs = {0: _draw(rng, (spec.T_P, H), 1.0), 1: _draw(rng, (spec.T_D, H), 1.0)}
+    w_gu_bits = np.empty((E_loc, 2 * I, H), np.uint16) if bf16 else None
+    w_dn_bits = np.empty((E_loc, H, I), np.uint16) if bf16 else None
 
-    w_gu, w_gu_bits = _quant(w_gu, spec.dtype)
-    w_dn, w_dn_bits = _quant(w_dn, spec.dtype)
-    x, x_bits = {}, {}
-    for ph, a in xs.items():
-        x[ph], x_bits[ph] = _quant(a, spec.dtype)
+    def expert(job):
+        kind, e = job
+        if kind == "gu":
+            v, b = _draw_block(seed, 1 + e, (2 * I, H), wstd, spec.dtype)
+            w_gu[e] = v
+            if bf16:
+                w_gu_bits[e] = b
+        else:
+            v, b = _draw_block(seed, 1 + E_loc + e, (H, I), wstd, spec.dtype)
+            w_dn[e] = v
+            if bf16:
+                w_dn_bits[e] = b
+
+    jobs = [("gu", e) for e in range(E_loc)] + [("dn", e) for e in range(E_loc)]
+    with cf.ThreadPoolExecutor(_POOL_WORKERS) as ex:
+        list(ex.map(expert, jobs))
+        fx = {ph: ex.submit(_draw_block, seed, 2 * E_loc + 1 + ph, ((spec.T_P, spec.T_D)[ph], H), 1.0, spec.dtype)
+              for ph in (0, 1)}
+        wg = _stream(seed, 0).standard_normal(size=(H, E), dtype=np.float32) * np.float32(wstd)
+        x, x_bits = {}, {}
+        for ph in (0, 1):
+            x[ph], x_bits[ph] = fx[ph].result()
     if bias is None:
         bias = np.zeros(E, np.float32)
     bias = np.asarray(bias, np.float32)
@@ -157,7 +177,7 @@ def make_layer(spec: LayerSpec, seed: int, bias: Optional[np.ndarray] = None) ->
         logits=logits,
         w_gu_bits=w_gu_bits,
         w_dn_bits=w_dn_bits,
-        x_bits=x_bits if spec.dtype == BF16 else None,
+        x_bits=x_bits if bf16 else None,
     )
 
 

@@ -1,0 +1,187 @@
+"""Helpers for the GPU tests: upload seeded inputs, drive the C ABI through
+the binding, read the phase-owned buffers back, compare with the oracle."""
+
+from __future__ import annotations
+
+import ctypes
+import math
+
+import numpy as np
+
+from synth import BF16, bf16_bits_to_f32
+
+_hip = None
+
+
+def hip():
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so")
+        _hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+        _hip.hipMemcpy.restype = ctypes.c_int
+    return _hip
+
+
+def read_dev(ptr: int, shape, dtype) -> np.ndarray:
+    """Copy device memory at `ptr` into a new host array (after a device sync)."""
+    a = np.empty(shape, dtype)
+    if a.nbytes == 0:
+        return a
+    st = hip().hipMemcpy(a.ctypes.data, ptr, a.nbytes, 2)  # device to host
+    assert st == 0, f"hipMemcpy failed ({st})"
+    return a
+
+
+def to_dev(a: np.ndarray):
+    import torch
+
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        t = torch.from_numpy(a.view(np.int16))
+    else:
+        t = torch.from_numpy(a)
+    return t.to("cuda")
+
+
+class GpuLayer:
+    """One context over a LayerInputs, with per-phase streams and outputs."""
+
+    def __init__(self, inp, max_tokens=None):
+        import torch
+
+        from paper_2609_00993_amd import moepd as M
+
+        self.M = M
+        self.inp = inp
+        spec = inp.spec
+        self.spec = spec
+        self.bf16 = spec.dtype == BF16
+        self.T = {0: spec.T_P, 1: spec.T_D}
+        if max_tokens is None:
+            max_tokens = (spec.T_P, spec.T_D)
+        self.w_gu = to_dev(inp.w_gu_bits if self.bf16 else inp.w_gu)
+        self.w_dn = to_dev(inp.w_dn_bits if self.bf16 else inp.w_dn)
+        self.x = {ph: to_dev(inp.x_bits[ph] if self.bf16 else inp.x[ph]) for ph in (0, 1)}
+        self.logits = {ph: to_dev(inp.logits[ph]) for ph in (0, 1)}
+        self.out = {ph: torch.zeros((self.T[ph], spec.H), dtype=torch.float32, device="cuda") for ph in (0, 1)}
+        cfg = M.make_config(spec.E, spec.e0, spec.E_loc, spec.k, spec.H, spec.I,
+                            M.MOE_DTYPE_BF16 if self.bf16 else M.MOE_DTYPE_F32, max_tokens[0], max_tokens[1])
+        st, self.ctx = M.moe_ctx_create(cfg, self.w_gu, self.w_dn)
+        M.check(st, "moe_ctx_create")
+        self.streams = {0: torch.cuda.Stream(), 1: torch.cuda.Stream()}
+
+    def run(self, ph, stream=None, T=None):
+        T = self.T[ph] if T is None else T
+        s = self.streams[ph] if stream is None else stream
+        self.M.layer(self.ctx, ph, self.logits[ph], T, self.x[ph], self.out[ph], s)
+
+    def fetch(self, ph):
+        import torch
+
+        torch.cuda.synchronize()
+        M, spec = self.M, self.spec
+        st, v = M.moe_phase_view(self.ctx, ph)
+        M.check(st)
+        T, k = v.tokens, spec.k
+        res = dict(
+            topk_idx=read_dev(v.topk_idx, (T, k), np.int32),
+            topk_w=read_dev(v.topk_w, (T, k), np.float32),
+            counts=read_dev(v.counts, (spec.E_loc,), np.int32),
+            offsets=read_dev(v.offsets, (spec.E_loc + 1,), np.int32),
+            row_of_slot=read_dev(v.row_of_slot, (T, k), np.int32),
+        )
+        R = int(res["offsets"][-1])
+        res["R"] = R
+        res["token_of_row"] = read_dev(v.token_of_row, (R,), np.int32)
+        edt = np.uint16 if self.bf16 else np.float32
+        res["x_perm_raw"] = read_dev(v.x_perm, (R, spec.H), edt)
+        res["h_raw"] = read_dev(v.h, (R, spec.I), edt)
+        res["y"] = read_dev(v.y, (R, spec.H), np.float32)
+        res["out"] = self.out[ph].cpu().numpy()
+        for key in ("x_perm", "h"):
+            raw = res[key + "_raw"]
+            res[key] = bf16_bits_to_f32(raw) if self.bf16 else raw
+        return res
+
+    def close(self):
+        if self.ctx:
+            self.M.check(self.M.moe_ctx_destroy(self.ctx))
+            self.ctx = None
+
+
+def rms(a) -> float:
+    a = np.asarray(a, np.float64)
+    return math.sqrt(float(np.mean(a * a))) if a.size else 0.0
+
+
+def tol_of(spec) -> float:
+    """Max |gpu - oracle| allowed on the layer output, as a fraction of the
+    oracle output's RMS: 2e-2 for bf16 layers, 1e-5 for float32 layers."""
+    return 2e-2 if spec.dtype == BF16 else 1e-5
+
+
+# Intermediate tensors have heavy tails (h = silu(g) u reaches ~20x its RMS),
+# so they are checked element by element against the precision they are
+# stored in rather than against the output's RMS bar:
+#  * bf16 h = RNE(h32): |h - h_ref| <= 2^-8 |h_ref| (half a bf16 ulp is at most
+#    2^-8 relative) + a floor of 1e-3 RMS for the float32 accumulation of g, u;
+#  * float32 y = h_bf16 W2^T: each h_i carries <= 2^-8 |h_i| error, so
+#    |y - y_ref| <= 2^-8 (|h_ref| |W2|^T) + 1e-3 RMS(y_ref);
+#  * float32 layers: |err| <= 1e-5 (|ref| + RMS(ref)) for h and y (float32
+#    accumulation over K <= 512 products, tails included).
+BF16_REL = 2.0 ** -8
+
+
+def assert_elementwise(got, ref, bound, what=""):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    if ref.size == 0:
+        return
+    err = np.abs(got - ref)
+    bad = err > bound
+    assert not bad.any(), (f"{what}: {int(bad.sum())} elements over the bound; worst excess "
+                           f"{float(np.max(err - bound)):.3e}")
+
+
+def check_h_y(res, ref, w_dn, offsets, spec, what=""):
+    """Check h and y of the GPU against the oracle's, element by element."""
+    h, y = res["h"], res["y"]
+    h_ref, y_ref = ref["h"], ref["y"]
+    if spec.dtype == BF16:
+        assert_elementwise(h, h_ref, BF16_REL * np.abs(h_ref) + 1e-3 * rms(h_ref), f"{what} h")
+        cond = np.zeros_like(y_ref)
+        ah = np.abs(h_ref)
+        for e in range(len(offsets) - 1):
+            a, b = int(offsets[e]), int(offsets[e + 1])
+            if a < b:
+                cond[a:b] = ah[a:b] @ np.abs(np.asarray(w_dn[e], np.float64)).T
+        assert_elementwise(y, y_ref, BF16_REL * cond + 1e-3 * rms(y_ref), f"{what} y")
+    else:
+        assert_elementwise(h, h_ref, 1e-5 * (np.abs(h_ref) + rms(h_ref)), f"{what} h")
+        assert_elementwise(y, y_ref, 1e-5 * (np.abs(y_ref) + rms(y_ref)), f"{what} y")
+
+
+# float32 gate weights: l_j - l_0 rounds (|diff| < 16 -> <= 1e-6 relative after
+# exp), expf and the k-term sum and divide add a few ulp: 2e-6 relative.
+W_RTOL = 2e-6
+
+
+def assert_route_layout_exact(res, ref, what=""):
+    assert np.array_equal(res["topk_idx"], ref["topk_idx"]), f"{what} topk_idx"
+    w, rw = res["topk_w"].astype(np.float64), ref["topk_w"]
+    err = np.abs(w - rw) / np.maximum(np.abs(rw), 1e-30)
+    assert err.size == 0 or err.max() <= W_RTOL, f"{what} topk_w rel err {err.max()}"
+    for key in ("counts", "offsets", "row_of_slot", "token_of_row"):
+        assert np.array_equal(res[key], ref[key]), f"{what} {key}"
+
+
+def assert_close_rms(got, ref, tol, what=""):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    if ref.size == 0:
+        return
+    scale = rms(ref)
+    err = float(np.max(np.abs(got - ref)))
+    assert err <= tol * scale, f"{what}: max|err| {err:.3e} > {tol:g} x rms {scale:.3e}"

@@ -1,0 +1,89 @@
+"""The C-ABI library loads and exports every function include/moepd.h declares,
+and its host-side validation answers without touching a GPU."""
+
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moepd.h")
+LIB = os.path.join(ROOT, "paper_2609_00993_amd", "libmoepd.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(moe_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_layer_calls():
+    names = declared_functions()
+    for n in ("moe_ctx_create", "moe_route", "moe_dispatch", "moe_expert_ffn", "moe_combine", "moe_phase_view",
+              "moe_phase_reset", "moe_ctx_destroy", "moe_status_string"):
+        assert n in names
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        pytest.fail("libmoepd.so is not built; run `python -m paper_2609_00993_amd.build`")
+    from paper_2609_00993_amd import moepd
+
+    return moepd
+
+
+def test_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], stdout=subprocess.PIPE, text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s(moe_\w+)$", out, flags=re.M))
+    declared = set(declared_functions())
+    assert declared <= exported, declared - exported
+    assert set(lib.SYMBOLS) == declared
+
+
+def test_status_strings(lib):
+    for code in range(-7, 1):
+        s = lib.moe_status_string(code)
+        assert s and s != "unknown status"
+    assert lib.moe_status_string(-99) == "unknown status"
+    assert lib.moe_kernel_name(lib.MOE_KERNEL_GEMM1) == "gemm1_swiglu"
+    assert lib.moe_kernel_name(99) == "?"
+
+
+def _cfg(lib, **kw):
+    base = dict(num_experts=8, expert_begin=0, num_local_experts=8, top_k=2, hidden=256, inter=512,
+                dtype=lib.MOE_DTYPE_F32, max_tokens_p=64, max_tokens_d=8)
+    base.update(kw)
+    return lib.make_config(**base)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(num_experts=0), dict(num_experts=2000), dict(num_local_experts=0), dict(num_local_experts=300),
+    dict(expert_begin=-1), dict(expert_begin=4), dict(top_k=0), dict(top_k=9), dict(top_k=17, num_experts=32,
+                                                                                  num_local_experts=32),
+    dict(hidden=100), dict(hidden=32), dict(inter=96), dict(dtype=7), dict(max_tokens_p=-1),
+    dict(max_tokens_d=(1 << 20) + 1), dict(flags=1),
+])
+def test_create_rejects_bad_config_without_gpu(lib, bad):
+    st, ctx = lib.moe_ctx_create(_cfg(lib, **bad), 0x1000, 0x2000)
+    assert st == lib.MOE_ERR_INVALID_ARG and ctx is None
+
+
+def test_create_rejects_null_weights(lib):
+    st, ctx = lib.moe_ctx_create(_cfg(lib), 0, 0x2000)
+    assert st == lib.MOE_ERR_INVALID_ARG and ctx is None
+    st, ctx = lib.moe_ctx_create(None, 0x1000, 0x2000)
+    assert st == lib.MOE_ERR_INVALID_ARG
+
+
+def test_null_context_calls(lib):
+    assert lib.moe_route(None, 0, 0, 0, 1) == lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_dispatch(None, 0, 0, 1) == lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_expert_ffn(None, 0, 1) == lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_combine(None, 0, 0, 1) == lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_phase_view(None, 0)[0] == lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_phase_reset(None, 0) == lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_timing_enable(None, 4) == lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_timing_read(None, 0, 0)[0] == lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_ctx_destroy(None) == lib.MOE_OK

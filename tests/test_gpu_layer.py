@@ -1,0 +1,245 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Exact: topk_idx, counts, offsets, row_of_slot, token_of_row, x_perm (a bit
+copy).  topk_w within 2e-6 relative.  The layer output within 2e-2 x RMS of
+the oracle's output for bf16 layers and 1e-5 x RMS for float32 layers; h and
+y element by element within the precision they are stored in (see
+tests/gpu_util.py).  The
+shapes below span several tiles, ragged tails and the degenerate cases
+(k = 1, k = E, empty batch, experts with no rows, experts off this GPU)."""
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import BF16, F32, LayerSpec, make_config, make_layer
+from tests.gpu_util import (GpuLayer, assert_close_rms, assert_route_layout_exact, check_h_y, tol_of)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def check_phase(g, inp, ph):
+    spec = inp.spec
+    res = g.fetch(ph)
+    ref = oracle.layer(inp.logits[ph], inp.x[ph], inp.w_gu, inp.w_dn, spec.k, spec.e0)
+    what = f"{spec.name} phase {ph}"
+    assert_route_layout_exact(res, ref, what)
+    assert np.array_equal(res["x_perm"], inp.x[ph][ref["token_of_row"]]), f"{what} x_perm"
+    check_h_y(res, ref, inp.w_dn, ref["offsets"], spec, what)
+    assert_close_rms(res["out"], ref["out"], tol_of(spec), f"{what} out")
+    # tokens without a resident slot are exact zeros
+    none = np.all(ref["row_of_slot"] < 0, axis=1)
+    assert np.all(res["out"][none] == 0)
+    return res
+
+
+SPECS = {
+    "cfg0-tiny-f32": lambda: make_config(0),
+    "cfg1-mid-bf16": lambda: make_config(1),
+    # E not a multiple of 64, e0 > 0, I and H not multiples of the n-tiles,
+    # a ragged token count, large-batch tiles for P and small-batch for D
+    "ragged-bf16": lambda: make_layer(LayerSpec("ragged-bf16", E=40, e0=5, E_loc=16, k=3, H=192, I=320, dtype=BF16,
+                                                T_P=1001, T_D=7), seed=11),
+    # small batches only (both phases on the weight-streaming tiles)
+    "skinny-bf16": lambda: make_layer(LayerSpec("skinny-bf16", E=64, e0=32, E_loc=32, k=2, H=256, I=128, dtype=BF16,
+                                                T_P=50, T_D=3), seed=12),
+    "k1-bf16": lambda: make_layer(LayerSpec("k1-bf16", E=16, e0=0, E_loc=16, k=1, H=128, I=128, dtype=BF16, T_P=900,
+                                            T_D=2), seed=13),
+    # k = E: every expert takes every token
+    "k-eq-E-bf16": lambda: make_layer(LayerSpec("kE-bf16", E=4, e0=0, E_loc=4, k=4, H=64, I=64, dtype=BF16, T_P=129,
+                                                T_D=1), seed=14),
+    # a pool above 256 experts (8 logits per lane), 64 resident, top-8
+    "wide-pool-bf16": lambda: make_layer(LayerSpec("wide-bf16", E=300, e0=100, E_loc=64, k=8, H=128, I=192,
+                                                   dtype=BF16, T_P=700, T_D=5), seed=15),
+    "ragged-f32": lambda: make_layer(LayerSpec("ragged-f32", E=12, e0=3, E_loc=6, k=2, H=192, I=128, dtype=F32,
+                                               T_P=77, T_D=0), seed=16),
+}
+
+
+@pytest.mark.parametrize("name", list(SPECS))
+def test_layer_parity(name):
+    inp = SPECS[name]()
+    print(f"[parity] {name}: {inp.spec}", flush=True)
+    g = GpuLayer(inp)
+    try:
+        for ph in (0, 1):
+            g.run(ph)
+        for ph in (0, 1):
+            check_phase(g, inp, ph)
+    finally:
+        g.close()
+
+
+def _snapshot(g, ph):
+    res = g.fetch(ph)
+    return {k: v.copy() for k, v in res.items() if isinstance(v, np.ndarray)}
+
+
+def test_concurrent_phases_bit_identical_to_solo():
+    """P and D enqueued on two streams at once give the same bits as each
+    phase run alone: the phases share only read-only weights."""
+    import torch
+
+    inp = make_config(1)
+    g = GpuLayer(inp)
+    try:
+        g.run(0)
+        p_solo = _snapshot(g, 0)
+        g.run(1)
+        d_solo = _snapshot(g, 1)
+        for rep in range(3):
+            g.run(0)
+            g.run(1)
+            torch.cuda.synchronize()
+            p, d = _snapshot(g, 0), _snapshot(g, 1)
+            for key in p_solo:
+                assert np.array_equal(p[key], p_solo[key]), (rep, "P", key)
+                assert np.array_equal(d[key], d_solo[key]), (rep, "D", key)
+        check_phase(g, inp, 0)
+        check_phase(g, inp, 1)
+    finally:
+        g.close()
+
+
+def test_phase_isolation():
+    """Running P never writes D's buffers (and the reverse): both phases own
+    disjoint allocations."""
+    inp = make_layer(LayerSpec("iso", E=16, e0=0, E_loc=16, k=2, H=128, I=128, dtype=BF16, T_P=400, T_D=9), seed=21)
+    g = GpuLayer(inp)
+    try:
+        M = g.M
+        g.run(1)
+        d0 = _snapshot(g, 1)
+        g.run(0)
+        d1 = _snapshot(g, 1)
+        for key in d0:
+            assert np.array_equal(d0[key], d1[key]), key
+        _, vp = M.moe_phase_view(g.ctx, 0)
+        _, vd = M.moe_phase_view(g.ctx, 1)
+        p_ptrs = [vp.topk_idx, vp.topk_w, vp.counts, vp.offsets, vp.row_of_slot, vp.token_of_row, vp.x_perm, vp.h, vp.y]
+        d_ptrs = [vd.topk_idx, vd.topk_w, vd.counts, vd.offsets, vd.row_of_slot, vd.token_of_row, vd.x_perm, vd.h, vd.y]
+        p_lo, p_hi = min(p_ptrs), max(p_ptrs)
+        d_lo, d_hi = min(d_ptrs), max(d_ptrs)
+        assert p_hi < d_lo or d_hi < p_lo
+        # D's addresses are fixed for the context's lifetime
+        g.run(1)
+        _, vd2 = M.moe_phase_view(g.ctx, 1)
+        assert (vd2.x_perm, vd2.h, vd2.y) == (vd.x_perm, vd.h, vd.y)
+    finally:
+        g.close()
+
+
+def test_repeat_is_deterministic():
+    inp = make_layer(LayerSpec("det", E=32, e0=0, E_loc=32, k=4, H=256, I=256, dtype=BF16, T_P=777, T_D=13), seed=22)
+    g = GpuLayer(inp)
+    try:
+        g.run(0)
+        a = _snapshot(g, 0)
+        g.run(0)
+        b = _snapshot(g, 0)
+        for key in a:
+            assert np.array_equal(a[key], b[key]), key
+    finally:
+        g.close()
+
+
+def test_state_machine_and_errors():
+    import torch
+
+    inp = make_layer(LayerSpec("sm", E=8, e0=0, E_loc=8, k=2, H=64, I=64, dtype=BF16, T_P=32, T_D=4), seed=23)
+    g = GpuLayer(inp)
+    M = g.M
+    try:
+        ctx, s = g.ctx, g.streams[0]
+        x, out, lg = g.x[0], g.out[0], g.logits[0]
+        assert M.moe_dispatch(ctx, 0, x, s) == M.MOE_ERR_STATE
+        assert M.moe_expert_ffn(ctx, 0, s) == M.MOE_ERR_STATE
+        assert M.moe_combine(ctx, 0, out, s) == M.MOE_ERR_STATE
+        assert M.moe_route(ctx, 2, lg, 32, s) == M.MOE_ERR_INVALID_PHASE
+        assert M.moe_route(ctx, -1, lg, 32, s) == M.MOE_ERR_INVALID_PHASE
+        assert M.moe_route(ctx, 0, lg, 33, s) == M.MOE_ERR_CAPACITY
+        assert M.moe_route(ctx, 1, g.logits[1], 5, s) == M.MOE_ERR_CAPACITY
+        assert M.moe_route(ctx, 0, lg, -1, s) == M.MOE_ERR_INVALID_ARG
+        assert M.moe_route(ctx, 0, 0, 32, s) == M.MOE_ERR_INVALID_ARG
+        assert M.moe_route(ctx, 0, lg, 32, 0) == M.MOE_ERR_INVALID_ARG  # no null stream
+        assert M.moe_route(ctx, 0, lg, 32, s) == M.MOE_OK
+        assert M.moe_route(ctx, 0, lg, 32, s) == M.MOE_ERR_STATE  # one pending op per phase
+        assert M.moe_phase_view(ctx, 0)[1].state == M.MOE_STATE_ROUTED
+        assert M.moe_phase_view(ctx, 1)[1].state == M.MOE_STATE_IDLE  # D untouched
+        assert M.moe_dispatch(ctx, 0, 0, s) == M.MOE_ERR_INVALID_ARG
+        assert M.moe_dispatch(ctx, 0, x, s) == M.MOE_OK
+        # cancellation: reset once the phase's work completed
+        torch.cuda.synchronize()
+        assert M.moe_phase_reset(ctx, 0) == M.MOE_OK
+        assert M.moe_phase_view(ctx, 0)[1].state == M.MOE_STATE_IDLE
+        # an empty batch is a legal no-work call and advances the phase
+        M.check(M.moe_route(ctx, 1, 0, 0, s))
+        M.check(M.moe_dispatch(ctx, 1, 0, s))
+        M.check(M.moe_expert_ffn(ctx, 1, s))
+        M.check(M.moe_combine(ctx, 1, 0, s))
+        torch.cuda.synchronize()
+        _, v = M.moe_phase_view(ctx, 1)
+        assert v.state == M.MOE_STATE_IDLE and v.tokens == 0
+        # a phase driven across two streams stays ordered
+        s2 = g.streams[1]
+        M.check(M.moe_route(ctx, 0, lg, 32, s))
+        M.check(M.moe_dispatch(ctx, 0, x, s2))
+        M.check(M.moe_expert_ffn(ctx, 0, s))
+        M.check(M.moe_combine(ctx, 0, out, s2))
+        check_phase(g, inp, 0)
+        # timing records
+        M.check(M.moe_timing_enable(ctx, 8))
+        g.run(0)
+        torch.cuda.synchronize()
+        st, ms, n = M.moe_timing_read(ctx, 0, M.MOE_KERNEL_GEMM1)
+        assert st == 0 and n == 1 and ms > 0
+        st, ms, n = M.moe_timing_read(ctx, 0, M.MOE_KERNEL_GEMM1)
+        assert st == 0 and n == 0
+        M.check(M.moe_timing_enable(ctx, 0))
+    finally:
+        g.close()
+
+
+def test_config2_full_size_sampled():
+    """The DeepSeek-V3-shaped share at its full size: routing and layout are
+    checked exactly for every token, x_perm bit-exactly, and the layer output
+    on a sample of tokens (a token's output depends on no other token, so the
+    oracle runs on the sampled sub-batch)."""
+    inp = make_config(2)
+    spec = inp.spec
+    g = GpuLayer(inp)
+    try:
+        g.run(0)
+        g.run(1)
+        for ph in (0, 1):
+            res = g.fetch(ph)
+            lg, x = inp.logits[ph], inp.x[ph]
+            idx, w = oracle.route(lg, spec.k)
+            le = oracle.local_map(idx, spec.e0, spec.E_loc)
+            counts, offsets, ros, tor = oracle.layout(le, spec.E_loc)
+            ref = dict(topk_idx=idx, topk_w=w, counts=counts, offsets=offsets, row_of_slot=ros, token_of_row=tor)
+            assert_route_layout_exact(res, ref, f"cfg2 phase {ph}")
+            assert np.array_equal(res["x_perm_raw"], inp.x_bits[ph][tor])
+            T = lg.shape[0]
+            rng = np.random.default_rng(100 + ph)
+            toks = np.sort(rng.choice(T, size=min(T, 40), replace=False))
+            sub = oracle.layer(lg[toks], x[toks], inp.w_gu, inp.w_dn, spec.k, spec.e0)
+            assert_close_rms(res["out"][toks], sub["out"], 2e-2, f"cfg2 phase {ph} out (sampled)")
+            # h and y of the sampled tokens' rows, reordered into the
+            # sub-batch's layout so that its offsets apply
+            kept = ros[toks] >= 0
+            rows_full = ros[toks][kept]
+            rows_sub = sub["row_of_slot"][kept]
+            order = np.argsort(rows_sub)
+            got = dict(h=res["h"][rows_full[order]], y=res["y"][rows_full[order]])
+            check_h_y(got, sub, inp.w_dn, sub["offsets"], spec, f"cfg2 phase {ph} (sampled rows)")
+    finally:
+        g.close()

@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--d-iters", type=int, default=60, help="D layers per latency measurement")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="instead of the layer, time a plain device copy of this many MiB (the reference kernel "
+                         "for scaling the HBM byte counters)")
     return ap.parse_args()
 
 
@@ -119,6 +122,30 @@ def cpu_baseline(inp, seconds):
     }
 
 
+def copy_calibration(args):
+    """A plain device-to-device copy of known size (reads and writes
+    copy_mib MiB each launch), timed with events on its stream."""
+    import torch
+
+    n = args.copy_mib * (1 << 20) // 4
+    src = torch.randn(n, device="cuda")
+    dst = torch.empty_like(src)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        for _ in range(max(1, args.warmup)):
+            dst.copy_(src)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        for _ in range(args.steps):
+            dst.copy_(src)
+        b.record(s)
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) * 1e3 / args.steps
+    by = 2 * n * 4
+    print(json.dumps({"mode": "copy", "bytes_read": n * 4, "bytes_written": n * 4, "mean_us": round(us, 2),
+                      "GB/s": round(by / (us * 1e-6) / 1e9, 1), "launches": args.steps + max(1, args.warmup)}))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -135,6 +162,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.copy_mib:
+        copy_calibration(args)
+        return
     dev = torch.device("cuda:0")
     inp = make_config(args.config)
     spec = inp.spec

@@ -92,8 +92,8 @@ enum { MOE_STATE_IDLE = 0, MOE_STATE_ROUTED = 1, MOE_STATE_DISPATCHED = 2, MOE_S
 /* Kernels whose launches can be timed (moe_timing_*). */
 enum {
   MOE_KERNEL_ROUTE = 0,   /* top-k gating */
-  MOE_KERNEL_COUNT = 1,   /* per-chunk expert histogram + prefix sum (dispatch notification) */
-  MOE_KERNEL_PLACE = 2,   /* stable row assignment (dispatch layout) */
+  MOE_KERNEL_COUNT = 1,   /* per-chunk expert histogram (dispatch notification) */
+  MOE_KERNEL_PLACE = 2,   /* prefix sum, counts/offsets and stable row assignment (dispatch layout) */
   MOE_KERNEL_PERMUTE = 3, /* token rows -> expert-contiguous rows (dispatch data movement) */
   MOE_KERNEL_GEMM1 = 4,   /* grouped gate/up GEMM with fused SwiGLU */
   MOE_KERNEL_GEMM2 = 5,   /* grouped down GEMM */

@@ -12,12 +12,13 @@ constexpr int kWave = 64;
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
-// Round to nearest, ties to even.  NaN stays NaN (quiet bit set).
+// Round to nearest, ties to even.  NaN stays NaN (quiet bit set).  Written
+// without branches so that epilogues converting many values stay straight-line.
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return uint16_t(u >> 16);
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t rne = u + 0x7fffu + ((u >> 16) & 1u);
+  const uint32_t r = ((u & 0x7fffffffu) > 0x7f800000u) ? (u | 0x00400000u) : rne;
+  return uint16_t(r >> 16);
 }
 
 // ---- wave utilities ----------------------------------------------------------

@@ -3,8 +3,8 @@
 //
 // Phase ownership follows Section 5.1 of the paper (table "Ownership in the
 // concurrent DeepEP runtime"): the weights are shared and read-only, while
-// each phase owns its buffers, counters (the dispatch arrival counter and
-// histogram cells), workspace and events, selected by an explicit phase id
+// each phase owns its buffers, counters (the dispatch histogram cells and
+// per-expert counts), workspace and events, selected by an explicit phase id
 // (Section 5.1, Section 6).  Each phase's buffers live in one allocation made
 // at creation, so their addresses never change (the D phase replays against
 // fixed addresses) and the two phases' address ranges are disjoint.  A phase
@@ -131,8 +131,7 @@ int alloc_phase(moe_ctx* ctx, int phase) {
   const size_t o_ros = take(slots * 4), o_tor = take(p.rows_cap * 4);
   const size_t o_xp = take(p.rows_cap * c.hidden * ctx->esz), o_h = take(p.rows_cap * c.inter * ctx->esz);
   const size_t o_y = take(p.rows_cap * c.hidden * 4);
-  const size_t o_cc = take((size_t)E * mc * 4), o_cb = take((size_t)E * mc * 4), o_tb = take((E + 1) * 4);
-  const size_t o_done = take(4);
+  const size_t o_cc = take((size_t)E * mc * 4), o_tb = take((E + 1) * 4);
 
   void* mem = nullptr;
   if (hipMalloc(&mem, off) != hipSuccess || !mem) {
@@ -151,10 +150,8 @@ int alloc_phase(moe_ctx* ctx, int phase) {
   p.b.h = base + o_h;
   p.b.y = (float*)(base + o_y);
   p.b.chunk_counts = (int32_t*)(base + o_cc);
-  p.b.chunk_base = (int32_t*)(base + o_cb);
   p.b.tile_base = (int32_t*)(base + o_tb);
-  p.b.done = (uint32_t*)(base + o_done);
-  // Zero the small metadata (counters, offsets, tile prefix) once at creation.
+  // Zero the small metadata (counts, offsets, tile prefix) once at creation.
   if (hipMemset(base + o_cnt, 0, o_ros - o_cnt) != hipSuccess) return MOE_ERR_HIP;
   if (hipMemset(base + o_tb, 0, off - o_tb) != hipSuccess) return MOE_ERR_HIP;
   if (hipEventCreateWithFlags(&p.ev, hipEventDisableTiming) != hipSuccess) {
@@ -271,14 +268,14 @@ int moe_dispatch(moe_ctx_t* ctx, int phase, const void* x, hipStream_t stream) {
     p.bm = ffn_f32_bm();
   }
   st = timed(p, MOE_KERNEL_COUNT, stream, [&] {
-    return launch_count(p.b.topk_idx, T, k, c.expert_begin, E_loc, p.chunk_tokens, p.nchunks, p.bm, p.b, stream);
+    return launch_count(p.b.topk_idx, T, k, c.expert_begin, E_loc, p.chunk_tokens, p.nchunks, p.b, stream);
+  });
+  if (st) return st;
+  st = timed(p, MOE_KERNEL_PLACE, stream, [&] {
+    return launch_place(p.b.topk_idx, T, k, c.expert_begin, E_loc, p.chunk_tokens, p.nchunks, p.bm, p.b, stream);
   });
   if (st) return st;
   if (T > 0) {
-    st = timed(p, MOE_KERNEL_PLACE, stream, [&] {
-      return launch_place(p.b.topk_idx, T, k, c.expert_begin, E_loc, p.chunk_tokens, p.nchunks, p.b, stream);
-    });
-    if (st) return st;
     st = timed(p, MOE_KERNEL_PERMUTE, stream, [&] {
       return launch_permute(x, T, k, c.hidden * ctx->esz, p.b.row_of_slot, p.b.x_perm, stream);
     });

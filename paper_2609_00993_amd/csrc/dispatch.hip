@@ -10,11 +10,12 @@
 // with LDS integer atomics (order-free), and ranks come from wave ballots
 // taken in slot order, so the layout is bit-exact and reproducible.
 //
-// Tokens are cut into chunks of `chunk_tokens`; the count kernel writes one
-// histogram cell per (expert, chunk) and its last block to arrive scans the
-// cells in expert-major order, which yields the first row of every
-// (expert, chunk) directly.  The place kernel then ranks the slots inside a
-// chunk and adds that base.
+// Tokens are cut into chunks of `chunk_tokens`.  The count kernel writes one
+// histogram cell per (expert, chunk).  The place kernel (the next launch, so
+// every cell is visible without device-scope fences) scans the cells in
+// expert-major order in LDS, which yields the first row of every (expert,
+// chunk) directly; its block 0 also publishes counts, offsets and the m-tile
+// prefix for the FFN.  Each block then ranks the slots of its own chunk.
 #include "common.h"
 #include "kernels.h"
 
@@ -44,91 +45,84 @@ __device__ __forceinline__ int block_exclusive_scan_256(int v, int* wave_tot, in
 }
 
 __global__ __launch_bounds__(256) void count_kernel(const int32_t* __restrict__ topk_idx, int T, int k, int e0,
-                                                    int e_loc, int chunk_tokens, int nchunks, int bm,
-                                                    PhaseBuffers b) {
+                                                    int e_loc, int chunk_tokens, int nchunks,
+                                                    int32_t* __restrict__ cells) {
   __shared__ int hist[kMaxLocalExperts];
-  __shared__ int cells[kMaxCells];
-  __shared__ int wave_tot[4];
-  __shared__ int is_last;
   const int tid = threadIdx.x;
   const int c = blockIdx.x;
-
   for (int i = tid; i < e_loc; i += 256) hist[i] = 0;
   __syncthreads();
   const long long s0 = (long long)c * chunk_tokens * k;
-  const long long t1 = min((long long)T, (long long)(c + 1) * chunk_tokens);
-  const long long s1 = t1 * k;
+  const long long s1 = min((long long)T, (long long)(c + 1) * chunk_tokens) * k;
   for (long long s = s0 + tid; s < s1; s += 256) {
     const int le = local_expert(topk_idx[s], e0, e_loc);
     if (le >= 0) atomicAdd(&hist[le], 1);
   }
   __syncthreads();
-  for (int i = tid; i < e_loc; i += 256) b.chunk_counts[i * nchunks + c] = hist[i];
+  for (int i = tid; i < e_loc; i += 256) cells[i * nchunks + c] = hist[i];
+}
 
-  // Publish the cells, then count arrivals; the last block does the scan.
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) is_last = (atomicAdd(b.done, 1u) == (unsigned)(nchunks - 1));
-  __syncthreads();
-  if (!is_last) return;
-  __threadfence();
+__global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ topk_idx, int T, int k, int e0,
+                                                    int e_loc, int chunk_tokens, int nchunks, int nbits, int bm,
+                                                    PhaseBuffers b) {
+  __shared__ int cells[kMaxCells];
+  __shared__ int base[kMaxLocalExperts];
+  __shared__ int run[kMaxLocalExperts + 1];
+  __shared__ int wcnt[4][kMaxLocalExperts + 1];
+  __shared__ int wave_tot[4];
+  const int tid = threadIdx.x, w = tid >> 6;
+  const int c = blockIdx.x;
 
+  // exclusive scan of all (expert, chunk) cells, expert-major
   const int n = e_loc * nchunks;  // <= kMaxCells (host guarantees)
-  for (int i = tid; i < n; i += 256) cells[i] = __atomic_load_n(&b.chunk_counts[i], __ATOMIC_RELAXED);
+  for (int i = tid; i < n; i += 256) cells[i] = b.chunk_counts[i];
   __syncthreads();
-  // each thread owns a contiguous segment of cells
   const int seg = (n + 255) / 256;
   const int lo = min(n, tid * seg), hi = min(n, lo + seg);
   int sum = 0;
   for (int i = lo; i < hi; ++i) sum += cells[i];
   int total;
-  int run = block_exclusive_scan_256(sum, wave_tot, &total);
+  int acc = block_exclusive_scan_256(sum, wave_tot, &total);
+  __syncthreads();  // every thread has read wave_tot; cells are rewritten below
   for (int i = lo; i < hi; ++i) {
     const int v = cells[i];
-    b.chunk_base[i] = run;
-    cells[i] = run;  // exclusive prefix, expert-major
-    run += v;
+    cells[i] = acc;
+    acc += v;
   }
   __syncthreads();
-  // offsets[e] = first row of (e, chunk 0); counts from consecutive offsets
-  for (int e = tid; e < e_loc; e += 256) {
-    const int off = cells[e * nchunks];
-    const int nxt = (e + 1 < e_loc) ? cells[(e + 1) * nchunks] : total;
-    b.offsets[e] = off;
-    b.counts[e] = nxt - off;
-    hist[e] = (nxt - off + bm - 1) / bm;  // m-tiles of expert e
-  }
-  if (tid == 0) b.offsets[e_loc] = total;
-  __syncthreads();
-  if (tid == 0) {
-    int acc = 0;
-    for (int e = 0; e < e_loc; ++e) {
-      b.tile_base[e] = acc;
-      acc += hist[e];
+  for (int e = tid; e < e_loc; e += 256) base[e] = cells[e * nchunks + c];
+  if (c == 0) {
+    // publish the dispatch shape: counts, offsets, m-tile prefix
+    for (int e = tid; e < e_loc; e += 256) {
+      const int off = cells[e * nchunks];
+      const int nxt = (e + 1 < e_loc) ? cells[(e + 1) * nchunks] : total;
+      b.offsets[e] = off;
+      b.counts[e] = nxt - off;
+      run[e] = (nxt - off + bm - 1) / bm;
     }
-    b.tile_base[e_loc] = acc;
-    __atomic_store_n(b.done, 0u, __ATOMIC_RELAXED);  // ready for the next call
+    __syncthreads();
+    if (tid == 0) {
+      b.offsets[e_loc] = total;
+      int t_acc = 0;
+      for (int e = 0; e < e_loc; ++e) {
+        b.tile_base[e] = t_acc;
+        t_acc += run[e];
+      }
+      b.tile_base[e_loc] = t_acc;
+    }
   }
-}
-
-__global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ topk_idx, int T, int k, int e0,
-                                                    int e_loc, int chunk_tokens, int nchunks, int nbits,
-                                                    PhaseBuffers b) {
-  __shared__ int run[kMaxLocalExperts + 1];
-  __shared__ int wcnt[4][kMaxLocalExperts + 1];
-  const int tid = threadIdx.x, w = tid >> 6;
-  const int c = blockIdx.x;
   for (int i = tid; i <= e_loc; i += 256) {
     run[i] = 0;
     wcnt[0][i] = wcnt[1][i] = wcnt[2][i] = wcnt[3][i] = 0;
   }
   __syncthreads();
+
+  // stable ranks of this chunk's slots, 256 slots per round, in slot order
   const long long s0 = (long long)c * chunk_tokens * k;
   const long long s1 = min((long long)T, (long long)(c + 1) * chunk_tokens) * k;
   const uint64_t lt = lanemask_lt();
-
-  for (long long base = s0; base < s1; base += 256) {
-    const long long s = base + tid;
+  for (long long sb = s0; sb < s1; sb += 256) {
+    const long long s = sb + tid;
     const bool valid = s < s1;
     const int le = valid ? local_expert(topk_idx[s], e0, e_loc) : -1;
     const int cat = le + 1;  // 0 = dropped or past the chunk
@@ -146,7 +140,7 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
       if (le >= 0) {
         int pre = run[cat];
         for (int v = 0; v < w; ++v) pre += wcnt[v][cat];
-        const int row = b.chunk_base[le * nchunks + c] + pre + rank;
+        const int row = base[le] + pre + rank;
         b.row_of_slot[s] = row;
         b.token_of_row[row] = (int)(s / k);
       } else {
@@ -162,66 +156,64 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
   }
 }
 
-// Token-major scatter: each 16-byte vector of x[t] is read once and written to
-// every row that t occupies, so HBM sees (tokens + rows) x row bytes.
-constexpr int kPermItems = 4;
+// Token-major scatter, one wave per token: lanes j < k read slot j's row, the
+// resident slots become a wave-uniform bit mask, and each 16-byte vector of
+// x[t] is read once and written to every row t occupies (row ids read back
+// as wave-uniform values).  Tokens with no resident slot are not read, so HBM
+// sees (tokens with a resident slot + rows) x row bytes.
+constexpr int kPermVec = 4;  // 16-byte vectors per lane per pass
 
-__global__ __launch_bounds__(256) void permute_kernel(const uint8_t* __restrict__ x, int T, int k, int nv,
-                                                      int tokens_per_block, const int32_t* __restrict__ row_of_slot,
-                                                      uint8_t* __restrict__ x_perm) {
-  const int t_begin = blockIdx.x * tokens_per_block;
-  const int t_end = min(T, t_begin + tokens_per_block);
-  const int items = (t_end - t_begin) * nv;
-  for (int base = 0; base < items; base += 256 * kPermItems) {
-    u32x4 v[kPermItems];
-    int tt[kPermItems], vi[kPermItems];
+__global__ __launch_bounds__(256) void permute_kernel(const u32x4* __restrict__ x, int T, int k, int nv,
+                                                      const int32_t* __restrict__ row_of_slot,
+                                                      u32x4* __restrict__ x_perm) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;  // whole wave leaves together
+  const int lane = threadIdx.x & 63;
+  const int r_l = lane < k ? row_of_slot[(size_t)t * k + lane] : -1;
+  const uint64_t resident = __ballot(r_l >= 0);
+  if (!resident) return;
+  const u32x4* xt = x + (size_t)t * nv;
+  for (int v0 = 0; v0 < nv; v0 += kWave * kPermVec) {
+    u32x4 a[kPermVec];
 #pragma unroll
-    for (int i = 0; i < kPermItems; ++i) {
-      const int it = base + i * 256 + (int)threadIdx.x;
-      tt[i] = -1;
-      if (it < items) {
-        const int tl = it / nv;
-        tt[i] = t_begin + tl;
-        vi[i] = it - tl * nv;
-        v[i] = load16(x + ((size_t)tt[i] * nv + vi[i]) * 16);
-      }
+    for (int i = 0; i < kPermVec; ++i) {
+      const int v = v0 + i * kWave + lane;
+      if (v < nv) a[i] = xt[v];
     }
+    uint64_t m = resident;
+    while (m) {
+      const int j = __builtin_ctzll(m);
+      m &= m - 1;
+      u32x4* dst = x_perm + (size_t)__builtin_amdgcn_readlane(r_l, j) * nv;
 #pragma unroll
-    for (int i = 0; i < kPermItems; ++i) {
-      if (tt[i] < 0) continue;
-      const int32_t* rs = row_of_slot + (size_t)tt[i] * k;
-      for (int j = 0; j < k; ++j) {
-        const int r = rs[j];
-        if (r >= 0) store16(x_perm + ((size_t)r * nv + vi[i]) * 16, v[i]);
+      for (int i = 0; i < kPermVec; ++i) {
+        const int v = v0 + i * kWave + lane;
+        if (v < nv) dst[v] = a[i];
       }
     }
   }
 }
 
 hipError_t launch_count(const int32_t* topk_idx, int T, int k, int e0, int e_loc, int chunk_tokens, int nchunks,
-                        int bm, const PhaseBuffers& b, hipStream_t s) {
-  count_kernel<<<dim3(nchunks), dim3(256), 0, s>>>(topk_idx, T, k, e0, e_loc, chunk_tokens, nchunks, bm, b);
+                        const PhaseBuffers& b, hipStream_t s) {
+  count_kernel<<<dim3(nchunks), dim3(256), 0, s>>>(topk_idx, T, k, e0, e_loc, chunk_tokens, nchunks,
+                                                   b.chunk_counts);
   return hipGetLastError();
 }
 
 hipError_t launch_place(const int32_t* topk_idx, int T, int k, int e0, int e_loc, int chunk_tokens, int nchunks,
-                        const PhaseBuffers& b, hipStream_t s) {
-  if (T <= 0) return hipSuccess;
+                        int bm, const PhaseBuffers& b, hipStream_t s) {
   int nbits = 0;
   while ((1 << nbits) <= e_loc) ++nbits;  // categories 0..e_loc
-  place_kernel<<<dim3(nchunks), dim3(256), 0, s>>>(topk_idx, T, k, e0, e_loc, chunk_tokens, nchunks, nbits, b);
+  place_kernel<<<dim3(nchunks), dim3(256), 0, s>>>(topk_idx, T, k, e0, e_loc, chunk_tokens, nchunks, nbits, bm, b);
   return hipGetLastError();
 }
 
 hipError_t launch_permute(const void* x, int T, int k, int row_bytes, const int32_t* row_of_slot, void* x_perm,
                           hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  const int nv = row_bytes / 16;
-  int tpb = 1024 / nv;
-  if (tpb < 1) tpb = 1;
-  const int grid = (T + tpb - 1) / tpb;
-  permute_kernel<<<dim3(grid), dim3(256), 0, s>>>((const uint8_t*)x, T, k, nv, tpb, row_of_slot,
-                                                  (uint8_t*)x_perm);
+  permute_kernel<<<dim3((T + 3) / 4), dim3(256), 0, s>>>((const u32x4*)x, T, k, row_bytes / 16, row_of_slot,
+                                                          (u32x4*)x_perm);
   return hipGetLastError();
 }
 

@@ -21,9 +21,18 @@ struct GemmArgsF {
   int e_loc, N, K, n_tiles, up_row;
 };
 
+// Tile of this workgroup (same schedule as the bf16 path); tile_base and
+// offsets are copied to LDS first so the search costs one memory latency.
 __device__ __forceinline__ bool tile_lookup_f(const GemmArgsF& g, int bm, int bn, int& e, int& m0, int& m_end,
                                               int& n0) {
-  const int total = g.tile_base[g.e_loc] * g.n_tiles;
+  __shared__ int s_tb[kMaxLocalExperts + 1];
+  __shared__ int s_off[kMaxLocalExperts + 1];
+  for (int i = threadIdx.x; i <= g.e_loc; i += blockDim.x) {
+    s_tb[i] = g.tile_base[i];
+    s_off[i] = g.offsets[i];
+  }
+  __syncthreads();
+  const int total = s_tb[g.e_loc] * g.n_tiles;
   const int per_xcd = (total + 7) >> 3;
   const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
   if (slot >= per_xcd) return false;
@@ -32,15 +41,15 @@ __device__ __forceinline__ bool tile_lookup_f(const GemmArgsF& g, int bm, int bn
   int lo = 0, hi = g.e_loc - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (g.tile_base[mid] * g.n_tiles <= L) lo = mid;
+    if (s_tb[mid] * g.n_tiles <= L) lo = mid;
     else hi = mid - 1;
   }
   e = lo;
-  const int mt_e = g.tile_base[e + 1] - g.tile_base[e];
-  const int local = L - g.tile_base[e] * g.n_tiles;
+  const int mt_e = s_tb[e + 1] - s_tb[e];
+  const int local = L - s_tb[e] * g.n_tiles;
   const int nt = local / mt_e, mt = local - nt * mt_e;
-  m0 = g.offsets[e] + mt * bm;
-  m_end = g.offsets[e + 1];
+  m0 = s_off[e] + mt * bm;
+  m_end = s_off[e + 1];
   n0 = nt * bn;
   return true;
 }

@@ -21,9 +21,7 @@ struct PhaseBuffers {
   float* y;               // [Rcap, H] float32
   // workspace
   int32_t* chunk_counts;  // [E_loc * max_chunks], expert-major
-  int32_t* chunk_base;    // [E_loc * max_chunks], first row of (expert, chunk)
   int32_t* tile_base;     // [E_loc + 1], prefix sum of m-tiles per expert
-  uint32_t* done;         // [1], arrival counter of the count kernel (returns to 0)
 };
 
 // Largest number of (expert, chunk) histogram cells the count kernel scans.
@@ -43,14 +41,15 @@ inline int dispatch_chunk_tokens(int T, int k, int e_loc) {
 hipError_t launch_route(const float* logits, int T, int E, int k, int32_t* topk_idx, float* topk_w,
                         hipStream_t s);
 
-// Histogram of each chunk's slots per local expert, then (last block) the
-// exclusive scan giving counts, offsets, chunk bases and m-tile prefix.
+// Histogram of each chunk's slots per local expert -> chunk_counts.
 hipError_t launch_count(const int32_t* topk_idx, int T, int k, int e0, int e_loc, int chunk_tokens, int nchunks,
-                        int bm, const PhaseBuffers& b, hipStream_t s);
-
-// Stable rows for every slot: row_of_slot and token_of_row.
-hipError_t launch_place(const int32_t* topk_idx, int T, int k, int e0, int e_loc, int chunk_tokens, int nchunks,
                         const PhaseBuffers& b, hipStream_t s);
+
+// Scan of the histogram cells (block 0 publishes counts, offsets and the
+// m-tile prefix for m-tiles of bm rows) and stable rows for every slot:
+// row_of_slot and token_of_row.  Launched for every batch, T = 0 included.
+hipError_t launch_place(const int32_t* topk_idx, int T, int k, int e0, int e_loc, int chunk_tokens, int nchunks,
+                        int bm, const PhaseBuffers& b, hipStream_t s);
 
 // x_perm[row] = x[t] for every resident slot (row-byte granularity 16 B).
 hipError_t launch_permute(const void* x, int T, int k, int row_bytes, const int32_t* row_of_slot, void* x_perm,

@@ -88,6 +88,23 @@ def kernel_units(spec, kernel, T, R, touched, esz):
     return 0, 0
 
 
+def recorded_traffic(cfg, phase, kernel):
+    """HBM bytes per launch of one kernel from the committed rocprofv3 counter
+    record (FETCH_SIZE + WRITE_SIZE, each scaled by a plain copy's reading),
+    or None when no record exists or a kernel source changed since."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        rec = json.load(open(path))
+        for rel, digest in rec["sources"].items():
+            if hashlib.sha256(open(os.path.join(ROOT, rel), "rb").read()).hexdigest() != digest:
+                return None
+        return rec["workloads"][f"cfg{cfg}"][f"{'P' if phase == 0 else 'D'}.{kernel}"]["hbm_bytes"]
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(inp, seconds):
     import numpy as np
 
@@ -282,7 +299,7 @@ def main():
         achieved = by / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = round(achieved / roof["peak"], 4)
-    roof["traffic"] = None
+    roof["traffic"] = recorded_traffic(args.config, ph_d, name_d)
     roof["kernel"] = f"{name_d} ({'P' if ph_d == 0 else 'D'})"
     roof["per_launch"] = {"bytes": by, "flops": fl, "mean_us": round(avg_s * 1e6, 2), "launches": n_d}
 

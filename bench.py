@@ -13,9 +13,11 @@ JSON line with:
 * d_latency_us: the D layer's GPU latency (events on the D stream) alone and
   while P layers keep the other stream busy, p50/p90/p99;
 * roofline: the kernel with the largest share of GPU time, its algorithmic
-  bytes or flops per launch over its mean launch duration (HIP events on the
-  stream it runs on, over the timed steps), against the MI355X peak that
-  bounds it;
+  bytes or flops per launch over its mean launch duration, against the MI355X
+  peak that bounds it.  Durations come from HIP events recorded around every
+  kernel on the stream it runs on, over a second pass of the same K timed
+  steps (the events themselves cost stream time, so the throughput pass runs
+  without them);
 * kernels: mean launch duration of every kernel of both phases;
 * cpu_baseline: the CPU oracle timed on a bounded sample on this host.
 """
@@ -214,8 +216,8 @@ def main():
         layer(1)
     torch.cuda.synchronize()
 
-    # ---- timed concurrent steps (per-kernel HIP events on the launching streams)
-    M.check(M.moe_timing_enable(ctx, args.steps), "moe_timing_enable")
+    # ---- timed concurrent steps: throughput (no per-kernel events, which
+    # would add a stream command around every kernel)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -223,6 +225,17 @@ def main():
         layer(1)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+
+    # ---- the same K concurrent steps again with per-kernel HIP events on the
+    # launching streams: per-kernel durations for the roofline
+    M.check(M.moe_timing_enable(ctx, args.steps), "moe_timing_enable")
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(args.steps):
+        layer(0)
+        layer(1)
+    torch.cuda.synchronize()
+    wall_events = time.perf_counter() - t1
     kern = {}
     for ph in (0, 1):
         for kid in range(M.MOE_NUM_KERNELS):
@@ -340,6 +353,7 @@ def main():
         },
         "roofline": roof,
         "kernels": kernels,
+        "kernels_pass_ms_per_step": round(wall_events / args.steps * 1e3, 4),
     }
     M.check(M.moe_ctx_destroy(ctx))
     if not args.no_cpu_baseline:

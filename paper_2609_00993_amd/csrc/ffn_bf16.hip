@@ -4,8 +4,9 @@
 //   h = silu(x_perm W1^T) * (x_perm W3^T), W1/W3 = rows [0,I)/[I,2I) of W_gu[e],
 // with the SwiGLU applied in the epilogue so g and u never reach memory.
 // GEMM2: y = h W2^T with W2 = W_dn[e].  h is rounded to bf16 (nearest even),
-// the operand type of GEMM2; y stays float32, the accumulation precision.  The paper's engine runs its own expert kernels (Section 7.1 states
-// BF16 and FP8 checkpoints); this is a gfx950 design of the same contraction.
+// the operand type of GEMM2; y stays float32, the accumulation precision.
+// The paper's engine runs its own expert kernels (Section 7.1 states BF16 and
+// FP8 checkpoints); this is a gfx950 design of the same contraction.
 //
 // Scheduling is fully device-side: the dispatch scan leaves tile_base, the
 // prefix sum of m-tiles per expert, and each workgroup finds its tile from
@@ -16,9 +17,11 @@
 // one expert that share a weight tile run side by side on one XCD's L2.
 //
 // Two tile shapes:
-//  * large batches (prefill): 256 threads, BMxBN output tile, K staged through
-//    LDS in 64-deep double-buffered slices (16-byte chunks, XOR-swizzled rows
-//    so the MFMA fragment reads are bank-conflict free), 32x32x16 MFMAs;
+//  * large batches (prefill): 256 threads, 128 x (128 gate + 128 up) or
+//    128 x 256 output tiles, 32x32x16 MFMAs.  Operands stream HBM -> LDS with
+//    global_load_lds_dwordx4 into a ring of three 64-deep K slices, so two
+//    slices are in flight while one is multiplied and no register or
+//    ds_write is spent on staging (see gemm_ring_body);
 //  * small batches (decode, a few rows per expert): the layer is a weight
 //    stream, so each wave reads its weight rows straight into MFMA operand
 //    registers (no LDS round trip), one 32-row m-tile and 32 columns per wave,
@@ -71,132 +74,14 @@ __device__ __forceinline__ bool tile_lookup(const GemmArgs& g, int bm, int bn, T
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const u32x4& u) { return __builtin_bit_cast(bf16x8_t, u); }
 
-__device__ __forceinline__ float silu_mul(float gt, float up) { return gt / (1.f + __expf(-gt)) * up; }
+// silu(g) * u for the bf16 h: the hardware reciprocal (about 1 ulp) is far
+// inside the bf16 rounding of h and avoids an IEEE division per element.
+__device__ __forceinline__ float silu_mul(float gt, float up) {
+  return gt * __builtin_amdgcn_rcpf(1.f + __expf(-gt)) * up;
+}
 
 // Row i of the 32x32 accumulator element r held by `lane` (column = lane & 31).
 __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
-
-// ------------------------------------------------------------------ tiled (prefill)
-
-template <int BM, int BN, int WM, int WN, bool GATED>
-__device__ __forceinline__ void gemm_tiled(const GemmArgs& g) {
-  constexpr int BK = 64;
-  constexpr int NT = WM * WN * 64;
-  constexpr int NB = GATED ? 2 : 1;
-  constexpr int BR = NB * BN;  // weight rows staged per tile
-  constexpr int WTM = BM / WM, WTN = BN / WN;
-  constexpr int FM = WTM / 32, FN = WTN / 32;
-  constexpr int AC = BM * 8 / NT, BC = BR * 8 / NT;  // 16-byte chunks per thread per slice
-  static_assert(FM * 32 == WTM && FN * 32 == WTN, "wave tile must be a multiple of 32x32");
-  static_assert(AC * NT == BM * 8 && BC * NT == BR * 8, "tile must split evenly over the threads");
-  __shared__ u32x4 As[2][BM * 8];
-  __shared__ u32x4 Bs[2][BR * 8];
-
-  TileCoord tc;
-  if (!tile_lookup(g, BM, BN, tc)) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const uint16_t* Be = g.B + (size_t)tc.e * g.b_stride;
-
-  const u32x4* a_src[AC];
-  int a_dst[AC];
-#pragma unroll
-  for (int i = 0; i < AC; ++i) {
-    const int q = tid + i * NT, r = q >> 3, c = q & 7;
-    const int row = min(tc.m0 + r, tc.m_end - 1);
-    a_src[i] = reinterpret_cast<const u32x4*>(g.A + (size_t)row * g.K) + c;
-    a_dst[i] = r * 8 + (c ^ (r & 7));
-  }
-  const u32x4* b_src[BC];
-  int b_dst[BC];
-#pragma unroll
-  for (int i = 0; i < BC; ++i) {
-    const int q = tid + i * NT, r = q >> 3, c = q & 7;
-    int brow;
-    if (GATED) brow = r < BN ? min(tc.n0 + r, g.N - 1) : g.up_row + min(tc.n0 + r - BN, g.N - 1);
-    else brow = min(tc.n0 + r, g.N - 1);
-    b_src[i] = reinterpret_cast<const u32x4*>(Be + (size_t)brow * g.K) + c;
-    b_dst[i] = r * 8 + (c ^ (r & 7));
-  }
-
-  u32x4 ra[AC], rb[BC];
-  f32x16_t acc[FM][FN * NB];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN * NB; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  const int KT = g.K / BK;
-#pragma unroll
-  for (int i = 0; i < AC; ++i) ra[i] = a_src[i][0];
-#pragma unroll
-  for (int i = 0; i < BC; ++i) rb[i] = b_src[i][0];
-#pragma unroll
-  for (int i = 0; i < AC; ++i) As[0][a_dst[i]] = ra[i];
-#pragma unroll
-  for (int i = 0; i < BC; ++i) Bs[0][b_dst[i]] = rb[i];
-  __syncthreads();
-
-  for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) {
-#pragma unroll
-      for (int i = 0; i < AC; ++i) ra[i] = a_src[i][(kt + 1) * 8];
-#pragma unroll
-      for (int i = 0; i < BC; ++i) rb[i] = b_src[i][(kt + 1) * 8];
-    }
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int ch = 2 * s + (lane >> 5);
-      bf16x8_t af[FM], bfr[FN * NB];
-#pragma unroll
-      for (int fm = 0; fm < FM; ++fm) {
-        const int r = wm * WTM + fm * 32 + (lane & 31);
-        af[fm] = as_bf16x8(As[cur][r * 8 + (ch ^ (r & 7))]);
-      }
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int fn = 0; fn < FN; ++fn) {
-          const int r = nb * BN + wn * WTN + fn * 32 + (lane & 31);
-          bfr[nb * FN + fn] = as_bf16x8(Bs[cur][r * 8 + (ch ^ (r & 7))]);
-        }
-#pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-        for (int j = 0; j < FN * NB; ++j)
-          acc[fm][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[fm], bfr[j], acc[fm][j], 0, 0, 0);
-    }
-    if (kt + 1 < KT) {
-#pragma unroll
-      for (int i = 0; i < AC; ++i) As[cur ^ 1][a_dst[i]] = ra[i];
-#pragma unroll
-      for (int i = 0; i < BC; ++i) Bs[cur ^ 1][b_dst[i]] = rb[i];
-    }
-    __syncthreads();
-  }
-
-  // epilogue
-#pragma unroll
-  for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-    for (int fn = 0; fn < FN; ++fn) {
-      const int col = tc.n0 + wn * WTN + fn * 32 + (lane & 31);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = tc.m0 + wm * WTM + fm * 32 + acc_row(r, lane);
-        if (row < tc.m_end && col < g.N) {
-          if (GATED)
-            static_cast<uint16_t*>(g.C)[(size_t)row * g.N + col] =
-                f32_to_bf16(silu_mul(acc[fm][fn][r], acc[fm][FN + fn][r]));
-          else
-            static_cast<float*>(g.C)[(size_t)row * g.N + col] = acc[fm][fn][r];
-        }
-      }
-    }
-}
 
 // ------------------------------------------------------------------ skinny (decode)
 
@@ -269,9 +154,205 @@ __device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
   }
 }
 
+#define MOEPD_GPTR(p) ((const void __attribute__((address_space(1)))*)(p))
+#define MOEPD_LPTR(p) ((void __attribute__((address_space(3)))*)(p))
+
+// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding:
+// vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] in bits [15:14]).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+
+// Wait until at most `newer` slices of NPS DMA instructions each are in
+// flight (newer <= MAXN, wave-uniform).
+template <int NPS, int MAXN>
+__device__ __forceinline__ void wait_slices(int newer) {
+  if constexpr (MAXN > 0) {
+    if (newer >= MAXN) {
+      wait_vmcnt<NPS * MAXN>();
+      return;
+    }
+    wait_slices<NPS, MAXN - 1>(newer);
+  } else {
+    wait_vmcnt<0>();
+  }
+}
+
+// The swizzle depends on the row length.
+// A staged row is BK bf16 = 2 BK bytes = CPR 16-byte chunks, and 256 / (2 BK)
+// rows share one 256-byte sweep of the 64 LDS banks.  Chunk c of row r is
+// stored at c ^ swz(r), swz(r) = (r / rows_per_sweep) % CPR, so the 16 lanes
+// that a ds_read_b128 serves together (16 consecutive rows, one chunk each)
+// cover all 64 banks once.
+template <int BK>
+__device__ __forceinline__ int swz(int row) {
+  constexpr int CPR = BK / 8, RPS = 256 / (2 * BK);
+  return (row / RPS) & (CPR - 1);
+}
+
+// Workgroup barrier without a memory fence; the signal fences keep the
+// compiler from moving LDS accesses across it.  Visibility of the DMA'd
+// stages is established by wait_vmcnt before the barrier.
+__device__ __forceinline__ void bare_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// One workgroup of 4 waves computes a BM x BN output tile of one expert.
+// Per BK-deep K slice it stages A (BM rows) and B (BR weight rows: BN gate +
+// BN up rows when GATED, BN rows otherwise) in LDS, swizzled as above.  The
+// slices travel HBM -> LDS by global_load_lds_dwordx4 (lane l of an
+// instruction lands 16 bytes at base + 16 l, so the swizzle is applied on the
+// global side), STAGES slices deep: the loads of slice kt + STAGES - 1 are
+// issued before slice kt is multiplied, and no register or ds_write is spent
+// on staging.  Only this wave's DMA instructions touch vmcnt inside the loop,
+// so wait_vmcnt(n * per-slice count) retires exactly the slices needed.
+//
+// Wave (wm, wn) of the WM x WN wave grid owns rows [wm WTM, +WTM) and output
+// columns [wn WTN, +WTN) (for GATED, the gate and the up column of the same
+// index, so the SwiGLU is applied in registers).  The K loop is branch-free:
+// rows past the expert's end are clamped to its last row and discarded at
+// the store, which keeps the MFMA and LDS-read schedule intact.
+template <int BM, int BR, int BK, int WM, int WN, bool GATED, int STAGES>
+__device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
+  constexpr int NB = GATED ? 2 : 1;
+  constexpr int BN = BR / NB;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int FM = WTM / 32, FN = WTN / 32;
+  constexpr int CPR = BK / 8;                      // 16-byte chunks per staged row
+  constexpr int RPI = 64 / CPR;                    // rows per DMA instruction (1 KB)
+  constexpr int A_INS = BM / RPI / 4, B_INS = BR / RPI / 4;  // per wave per slice
+  constexpr int NPS = A_INS + B_INS;               // vector-memory ops per wave per slice
+  constexpr int A_CH = BM * CPR, B_CH = BR * CPR;  // 16-byte chunks per slice
+  static_assert(WM * WN == 4, "four waves");
+  static_assert(BK == 32 || BK == 64, "slice depth");
+  static_assert(A_INS * RPI * 4 == BM && B_INS * RPI * 4 == BR, "slices split into whole DMA instructions");
+  static_assert(FM * 32 == WTM && FN * 32 == WTN, "wave tile must be a multiple of 32x32");
+  static_assert(STAGES >= 2 && NPS * (STAGES - 2) < 64, "pipeline depth");
+  __shared__ u32x4 ring[STAGES][A_CH + B_CH];
+
+  TileCoord tc;
+  if (!tile_lookup(g, BM, BN, tc)) return;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+  const uint16_t* Be = g.B + (size_t)tc.e * g.b_stride;
+
+  // Per-lane source rows of this wave's DMA instructions; lane l fills LDS
+  // chunk l of its instruction: row r = RPI i + l / CPR, physical chunk
+  // l % CPR, so it loads logical chunk (l % CPR) ^ swz(r).
+  const int lrow = lane / CPR, lphys = lane % CPR;
+  const uint16_t* a_src[A_INS];
+#pragma unroll
+  for (int i = 0; i < A_INS; ++i) {
+    const int r = (wave * A_INS + i) * RPI + lrow;
+    a_src[i] = g.A + (size_t)min(tc.m0 + r, tc.m_end - 1) * g.K + (lphys ^ swz<BK>(r)) * 8;
+  }
+  const uint16_t* b_src[B_INS];
+#pragma unroll
+  for (int i = 0; i < B_INS; ++i) {
+    const int r = (wave * B_INS + i) * RPI + lrow;
+    int brow;
+    if (GATED) brow = r < BN ? min(tc.n0 + r, g.N - 1) : g.up_row + min(tc.n0 + r - BN, g.N - 1);
+    else brow = min(tc.n0 + r, g.N - 1);
+    b_src[i] = Be + (size_t)brow * g.K + (lphys ^ swz<BK>(r)) * 8;
+  }
+
+  auto issue = [&](int kt, int slot) {
+    const int koff = kt * BK;
+#pragma unroll
+    for (int i = 0; i < A_INS; ++i)
+      __builtin_amdgcn_global_load_lds(MOEPD_GPTR(a_src[i] + koff), MOEPD_LPTR(&ring[slot][(wave * A_INS + i) * 64]),
+                                       16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < B_INS; ++i)
+      __builtin_amdgcn_global_load_lds(MOEPD_GPTR(b_src[i] + koff),
+                                       MOEPD_LPTR(&ring[slot][A_CH + (wave * B_INS + i) * 64]), 16, 0, 0);
+  };
+
+  f32x16_t acc[FM][FN * NB];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN * NB; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  // 32-row blocks of this wave that hold rows of the expert (wave-uniform)
+
+  const int KT = g.K / BK;
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < KT) issue(st, st);
+
+  int slot = 0;
+  for (int kt = 0; kt < KT; ++kt) {
+    // slice kt has landed once at most (newer slices issued) * NPS ops remain
+    wait_slices<NPS, STAGES - 2>(min(KT - 1 - kt, STAGES - 2));
+    bare_barrier();  // every wave's part of slice kt is in LDS; slot of kt-1 is free
+    if (kt + STAGES - 1 < KT) {
+      int ns = slot + STAGES - 1;
+      if (ns >= STAGES) ns -= STAGES;
+      issue(kt + STAGES - 1, ns);
+    }
+    const u32x4* As = &ring[slot][0];
+    const u32x4* Bs = &ring[slot][A_CH];
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s) {
+      const int ch = 2 * s + (lane >> 5);
+      bf16x8_t af[FM], bfr[FN * NB];
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) {
+        const int r = wm * WTM + fm * 32 + (lane & 31);
+        af[fm] = as_bf16x8(As[r * CPR + (ch ^ swz<BK>(r))]);
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+          const int r = nb * BN + wn * WTN + fn * 32 + (lane & 31);
+          bfr[nb * FN + fn] = as_bf16x8(Bs[r * CPR + (ch ^ swz<BK>(r))]);
+        }
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int j = 0; j < FN * NB; ++j)
+          acc[fm][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[fm], bfr[j], acc[fm][j], 0, 0, 0);
+    }
+    if (++slot == STAGES) slot = 0;
+  }
+
+  // epilogue: SwiGLU -> bf16 h, or float32 y.  Rows are checked once per
+  // 32-row block; only the expert's last block checks each row.
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    const int rb = tc.m0 + wm * WTM + fm * 32;
+    if (rb >= tc.m_end) continue;
+    const bool full = rb + 32 <= tc.m_end;
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const int col = tc.n0 + wn * WTN + fn * 32 + (lane & 31);
+      if (col >= g.N) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int ro = acc_row(r, lane);
+        if (full || rb + ro < tc.m_end) {
+          const size_t at = (size_t)(rb + ro) * g.N + col;
+          if (GATED)
+            static_cast<uint16_t*>(g.C)[at] = f32_to_bf16(silu_mul(acc[fm][fn][r], acc[fm][FN + fn][r]));
+          else
+            static_cast<float*>(g.C)[at] = acc[fm][fn][r];
+        }
+      }
+    }
+  }
+}
+
 // Distinct entry points so that profiles name each GEMM of each regime.
-__global__ __launch_bounds__(256) void gemm1_swiglu_prefill(GemmArgs g) { gemm_tiled<128, 128, 2, 2, true>(g); }
-__global__ __launch_bounds__(256) void gemm2_down_prefill(GemmArgs g) { gemm_tiled<128, 256, 2, 2, false>(g); }
+__global__ __launch_bounds__(256) void gemm1_swiglu_prefill(GemmArgs g) { gemm_ring_body<128, 256, 64, 2, 2, true, 3>(g); }
+__global__ __launch_bounds__(256) void gemm2_down_prefill(GemmArgs g) { gemm_ring_body<128, 256, 64, 2, 2, false, 3>(g); }
 __global__ __launch_bounds__(256) void gemm1_swiglu_decode(GemmArgs g) { gemm_skinny<true>(g); }
 __global__ __launch_bounds__(256) void gemm2_down_decode(GemmArgs g) { gemm_skinny<false>(g); }
 

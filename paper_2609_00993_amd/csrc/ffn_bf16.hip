@@ -25,7 +25,7 @@
 //  * small batches (decode, a few rows per expert): the layer is a weight
 //    stream, so each wave reads its weight rows straight into MFMA operand
 //    registers (no LDS round trip), one 32-row m-tile and 32 columns per wave,
-//    with the next K slice in flight while the current one is multiplied.
+//    with the next two 64-deep K blocks in flight while one is multiplied.
 #include "common.h"
 #include "kernels.h"
 
@@ -111,32 +111,31 @@ __device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
     for (int q = 0; q < 16; ++q) acc[j][q] = 0.f;
 
   const int KB = g.K / 64;
-  u32x4 a0[4], b0[NB][4], a1[4], b1[NB][4];
-#pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    a0[s] = pa[s];
-#pragma unroll
-    for (int j = 0; j < NB; ++j) b0[j][s] = pb[j][s];
-  }
-  for (int kb = 0; kb < KB; ++kb) {
-    if (kb + 1 < KB) {
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        a1[s] = pa[(kb + 1) * 8 + s];
-#pragma unroll
-        for (int j = 0; j < NB; ++j) b1[j][s] = pb[j][(kb + 1) * 8 + s];
-      }
-    }
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-      for (int j = 0; j < NB; ++j)
-        acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a0[s]), as_bf16x8(b0[j][s]), acc[j], 0, 0, 0);
+  constexpr int PF = 2;  // 64-deep K blocks in flight per wave (a static register ring)
+  u32x4 ra[PF][4], rb[PF][NB][4];
+  auto load = [&](int kb, u32x4 (&a)[4], u32x4 (&b)[NB][4]) {
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      a0[s] = a1[s];
+      a[s] = pa[kb * 8 + s];
 #pragma unroll
-      for (int j = 0; j < NB; ++j) b0[j][s] = b1[j][s];
+      for (int j = 0; j < NB; ++j) b[j][s] = pb[j][kb * 8 + s];
+    }
+  };
+#pragma unroll
+  for (int p = 0; p < PF; ++p)
+    if (p < KB) load(p, ra[p], rb[p]);
+  for (int kb0 = 0; kb0 < KB; kb0 += PF) {
+#pragma unroll
+    for (int p = 0; p < PF; ++p) {
+      const int kb = kb0 + p;
+      if (kb < KB) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(ra[p][s]), as_bf16x8(rb[p][j][s]), acc[j], 0, 0, 0);
+        if (kb + PF < KB) load(kb + PF, ra[p], rb[p]);
+      }
     }
   }
 

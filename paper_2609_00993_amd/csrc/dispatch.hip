@@ -65,10 +65,14 @@ __global__ __launch_bounds__(256) void count_kernel(const int32_t* __restrict__ 
 __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ topk_idx, int T, int k, int e0,
                                                     int e_loc, int chunk_tokens, int nchunks, int nbits, int bm,
                                                     PhaseBuffers b) {
-  __shared__ int cells[kMaxCells];
-  __shared__ int base[kMaxLocalExperts];
-  __shared__ int run[kMaxLocalExperts + 1];
-  __shared__ int wcnt[4][kMaxLocalExperts + 1];
+  // LDS: the cells (sized at launch to e_loc * nchunks, so a small batch
+  // needs only a few KB and can share a CU with a running prefill GEMM),
+  // then per-expert bases, running counts and per-wave counts.
+  extern __shared__ int lds_dyn[];
+  int* cells = lds_dyn;
+  int* base = cells + e_loc * nchunks;
+  int* run = base + e_loc;
+  int(*wcnt)[kMaxLocalExperts + 1] = reinterpret_cast<int(*)[kMaxLocalExperts + 1]>(run + e_loc + 1);
   __shared__ int wave_tot[4];
   const int tid = threadIdx.x, w = tid >> 6;
   const int c = blockIdx.x;
@@ -205,7 +209,8 @@ hipError_t launch_place(const int32_t* topk_idx, int T, int k, int e0, int e_loc
                         int bm, const PhaseBuffers& b, hipStream_t s) {
   int nbits = 0;
   while ((1 << nbits) <= e_loc) ++nbits;  // categories 0..e_loc
-  place_kernel<<<dim3(nchunks), dim3(256), 0, s>>>(topk_idx, T, k, e0, e_loc, chunk_tokens, nchunks, nbits, bm, b);
+  const size_t lds = sizeof(int) * ((size_t)e_loc * nchunks + e_loc + (e_loc + 1) + 4 * (kMaxLocalExperts + 1));
+  place_kernel<<<dim3(nchunks), dim3(256), lds, s>>>(topk_idx, T, k, e0, e_loc, chunk_tokens, nchunks, nbits, bm, b);
   return hipGetLastError();
 }
 

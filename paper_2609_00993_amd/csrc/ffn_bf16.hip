@@ -19,13 +19,15 @@
 // Two tile shapes:
 //  * large batches (prefill): 256 threads, 128 x (128 gate + 128 up) or
 //    128 x 256 output tiles, 32x32x16 MFMAs.  Operands stream HBM -> LDS with
-//    global_load_lds_dwordx4 into a ring of three 64-deep K slices, so two
-//    slices are in flight while one is multiplied and no register or
-//    ds_write is spent on staging (see gemm_ring_body);
+//    global_load_lds_dwordx4 into a ring of three 64-deep K slices; fragments
+//    are double-buffered in registers and the LDS reads and DMA issues are
+//    interleaved with the MFMAs (see gemm_ring_body);
 //  * small batches (decode, a few rows per expert): the layer is a weight
 //    stream, so each wave reads its weight rows straight into MFMA operand
 //    registers (no LDS round trip), one 32-row m-tile and 32 columns per wave,
 //    with the next two 64-deep K blocks in flight while one is multiplied.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -48,13 +50,8 @@ struct TileCoord {
   int e, m0, m_end, n0;
 };
 
-__device__ __forceinline__ bool tile_lookup(const GemmArgs& g, int bm, int bn, TileCoord& tc) {
-  const int total = g.tile_base[g.e_loc] * g.n_tiles;
-  const int per_xcd = (total + 7) >> 3;
-  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-  if (slot >= per_xcd) return false;
-  const int L = xcd * per_xcd + slot;
-  if (L >= total) return false;
+// Coordinates of logical tile L (expert-major, then n-tile, then m-tile).
+__device__ __forceinline__ void tile_at(const GemmArgs& g, int L, int bm, int bn, TileCoord& tc) {
   int lo = 0, hi = g.e_loc - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
@@ -69,7 +66,31 @@ __device__ __forceinline__ bool tile_lookup(const GemmArgs& g, int bm, int bn, T
   tc.m0 = g.offsets[e] + mt * bm;
   tc.m_end = g.offsets[e + 1];
   tc.n0 = nt * bn;
-  return true;
+}
+
+// Logical tile of this workgroup, or -1.  The dispatcher deals workgroups
+// round-robin to the 8 XCDs; XCD x takes the logical tiles
+// [x per_xcd, (x+1) per_xcd), so the tiles that share an expert's weights
+// run side by side on one XCD's L2.  The grid, a multiple of 8 and at least
+// the largest possible tile count, covers every tile.
+__device__ __forceinline__ int block_tile(const GemmArgs& g) {
+  const int total = g.tile_base[g.e_loc] * g.n_tiles;
+  const int per_xcd = (total + 7) >> 3;
+  const int slot = blockIdx.x >> 3;
+  if (slot >= per_xcd) return -1;
+  const int L = (blockIdx.x & 7) * per_xcd + slot;
+  return L < total ? L : -1;
+}
+
+// First 64-deep K block of a decode tile (of nk blocks).  When a row of K
+// bf16 values is a multiple of 4 KB (K % 2048 == 0), every weight row starts
+// on the same memory channel, so tiles that stream the same K offset at the
+// same time press on a few channels; rotating the start by the tile's
+// (expert, n-tile) index spreads them.  Other pitches already spread and
+// keep the plain order (the launch picks the variant), which measured faster
+// for them.
+__device__ __forceinline__ int k_rotation(const TileCoord& tc, int n_tiles, int bn, int nk) {
+  return (int)((unsigned)((tc.e * n_tiles + tc.n0 / bn) * 2) % (unsigned)nk);
 }
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const u32x4& u) { return __builtin_bit_cast(bf16x8_t, u); }
@@ -85,12 +106,9 @@ __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 
 
 // ------------------------------------------------------------------ skinny (decode)
 
-template <bool GATED>
-__device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
-  constexpr int BM = 32, BN = 128;
+template <bool GATED, bool ROT>
+__device__ __forceinline__ void gemm_skinny_tile(const GemmArgs& g, const TileCoord& tc) {
   constexpr int NB = GATED ? 2 : 1;
-  TileCoord tc;
-  if (!tile_lookup(g, BM, BN, tc)) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 31, kg = lane >> 5;
   const int arow = min(tc.m0 + r, tc.m_end - 1);
@@ -111,9 +129,14 @@ __device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
     for (int q = 0; q < 16; ++q) acc[j][q] = 0.f;
 
   const int KB = g.K / 64;
+  const int krot = ROT ? k_rotation(tc, g.n_tiles, 128, KB) : 0;
   constexpr int PF = 2;  // 64-deep K blocks in flight per wave (a static register ring)
   u32x4 ra[PF][4], rb[PF][NB][4];
   auto load = [&](int kb, u32x4 (&a)[4], u32x4 (&b)[NB][4]) {
+    if (ROT) {
+      kb += krot;
+      if (kb >= KB) kb -= KB;
+    }
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       a[s] = pa[kb * 8 + s];
@@ -151,6 +174,16 @@ __device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
       }
     }
   }
+}
+
+template <bool GATED, bool ROT>
+__device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
+  constexpr int BM = 32, BN = 128;
+  const int L = block_tile(g);
+  if (L < 0) return;
+  TileCoord tc;
+  tile_at(g, L, BM, BN, tc);
+  gemm_skinny_tile<GATED, ROT>(g, tc);
 }
 
 #define MOEPD_GPTR(p) ((const void __attribute__((address_space(1)))*)(p))
@@ -200,15 +233,71 @@ __device__ __forceinline__ void bare_barrier() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+// s_waitcnt vmcnt(n) lgkmcnt(0): this wave's LDS reads are done and at most
+// n of its vector-memory operations are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x70);
+}
+
+template <int NPS, int MAXN>
+__device__ __forceinline__ void wait_slices_lgkm0(int newer) {
+  if constexpr (MAXN > 0) {
+    if (newer >= MAXN) {
+      wait_vmcnt_lgkm0<NPS * MAXN>();
+      return;
+    }
+    wait_slices_lgkm0<NPS, MAXN - 1>(newer);
+  } else {
+    wait_vmcnt_lgkm0<0>();
+  }
+}
+
+// Scheduling-group masks of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008, kSchedVmem = 0x010, kSchedDsRead = 0x100;
+
+// Ask the scheduler for N MFMAs with NR LDS reads spread over the first half
+// of them (so the reads have the second half to land before the next
+// substep needs them) and NV vector-memory instructions over the second
+// half (sync group SYNC).
+template <int I, int N, int NV, int NR, int SYNC>
+__device__ __forceinline__ void interleave() {
+  if constexpr (I < N) {
+    constexpr int H = (N + 1) / 2;
+    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, SYNC);
+    if constexpr (I < H) {
+      constexpr int r = NR * (I + 1) / H - NR * I / H;
+      if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, r, SYNC);
+    } else {
+      constexpr int v = NV * (I - H + 1) / (N - H) - NV * (I - H) / (N - H);
+      if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(kSchedVmem, v, SYNC);
+    }
+    interleave<I + 1, N, NV, NR, SYNC>();
+  }
+}
+
 // One workgroup of 4 waves computes a BM x BN output tile of one expert.
 // Per BK-deep K slice it stages A (BM rows) and B (BR weight rows: BN gate +
 // BN up rows when GATED, BN rows otherwise) in LDS, swizzled as above.  The
 // slices travel HBM -> LDS by global_load_lds_dwordx4 (lane l of an
 // instruction lands 16 bytes at base + 16 l, so the swizzle is applied on the
-// global side), STAGES slices deep: the loads of slice kt + STAGES - 1 are
-// issued before slice kt is multiplied, and no register or ds_write is spent
-// on staging.  Only this wave's DMA instructions touch vmcnt inside the loop,
-// so wait_vmcnt(n * per-slice count) retires exactly the slices needed.
+// global side) into a ring of STAGES slots; no register or ds_write is spent
+// on staging.
+//
+// The pipeline has three levels:
+//  * DMA: once every wave has read slice kt out of its slot (the barrier at
+//    the end of slice kt), slice kt + STAGES is issued into that slot, so
+//    STAGES - 1 slices are in flight while one is multiplied.  Only this
+//    wave's DMA instructions (and older stores) count in vmcnt, and loads
+//    complete in order, so wait_vmcnt(n * per-slice count) retires exactly
+//    the slices needed;
+//  * fragments: each 16-deep substep's A/B fragments are read from LDS into
+//    one of two register sets while the MFMAs of the previous substep run on
+//    the other (the read of a slice's first substep crosses the barrier);
+//  * instructions: scheduling-group barriers spread the LDS reads and DMA
+//    issues between the MFMAs, so the single wave per SIMD never waits on
+//    its own reads.
 //
 // Wave (wm, wn) of the WM x WN wave grid owns rows [wm WTM, +WTM) and output
 // columns [wn WTN, +WTN) (for GATED, the gate and the up column of the same
@@ -220,46 +309,49 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   constexpr int NB = GATED ? 2 : 1;
   constexpr int BN = BR / NB;
   constexpr int WTM = BM / WM, WTN = BN / WN;
-  constexpr int FM = WTM / 32, FN = WTN / 32;
+  constexpr int FM = WTM / 32, FN = WTN / 32, FB = FN * NB;
+  constexpr int SUB = BK / 16;                     // MFMA K steps per slice
   constexpr int CPR = BK / 8;                      // 16-byte chunks per staged row
   constexpr int RPI = 64 / CPR;                    // rows per DMA instruction (1 KB)
   constexpr int A_INS = BM / RPI / 4, B_INS = BR / RPI / 4;  // per wave per slice
   constexpr int NPS = A_INS + B_INS;               // vector-memory ops per wave per slice
   constexpr int A_CH = BM * CPR, B_CH = BR * CPR;  // 16-byte chunks per slice
+  constexpr int NRD = FM + FB, NMF = FM * FB;      // LDS reads and MFMAs per substep
   static_assert(WM * WN == 4, "four waves");
   static_assert(BK == 32 || BK == 64, "slice depth");
+  static_assert(SUB % 2 == 0, "fragment double buffer alternates within a slice");
   static_assert(A_INS * RPI * 4 == BM && B_INS * RPI * 4 == BR, "slices split into whole DMA instructions");
   static_assert(FM * 32 == WTM && FN * 32 == WTN, "wave tile must be a multiple of 32x32");
-  static_assert(STAGES >= 2 && NPS * (STAGES - 2) < 64, "pipeline depth");
+  static_assert(STAGES >= 2 && NPS * (STAGES - 1) < 64, "pipeline depth");
   __shared__ u32x4 ring[STAGES][A_CH + B_CH];
 
-  TileCoord tc;
-  if (!tile_lookup(g, BM, BN, tc)) return;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / WN, wn = wave % WN;
-  const uint16_t* Be = g.B + (size_t)tc.e * g.b_stride;
-
-  // Per-lane source rows of this wave's DMA instructions; lane l fills LDS
-  // chunk l of its instruction: row r = RPI i + l / CPR, physical chunk
-  // l % CPR, so it loads logical chunk (l % CPR) ^ swz(r).
+  const int KT = g.K / BK;
+  // Per-lane DMA source rows: lane l fills LDS chunk l of its instruction,
+  // row r = RPI i + l / CPR, physical chunk l % CPR, so it loads logical
+  // chunk (l % CPR) ^ swz(r).
   const int lrow = lane / CPR, lphys = lane % CPR;
-  const uint16_t* a_src[A_INS];
-#pragma unroll
-  for (int i = 0; i < A_INS; ++i) {
-    const int r = (wave * A_INS + i) * RPI + lrow;
-    a_src[i] = g.A + (size_t)min(tc.m0 + r, tc.m_end - 1) * g.K + (lphys ^ swz<BK>(r)) * 8;
-  }
-  const uint16_t* b_src[B_INS];
-#pragma unroll
-  for (int i = 0; i < B_INS; ++i) {
-    const int r = (wave * B_INS + i) * RPI + lrow;
-    int brow;
-    if (GATED) brow = r < BN ? min(tc.n0 + r, g.N - 1) : g.up_row + min(tc.n0 + r - BN, g.N - 1);
-    else brow = min(tc.n0 + r, g.N - 1);
-    b_src[i] = Be + (size_t)brow * g.K + (lphys ^ swz<BK>(r)) * 8;
-  }
 
+  const uint16_t* a_src[A_INS];
+  const uint16_t* b_src[B_INS];
+  auto set_sources = [&](const TileCoord& tc) {
+    const uint16_t* Be = g.B + (size_t)tc.e * g.b_stride;
+#pragma unroll
+    for (int i = 0; i < A_INS; ++i) {
+      const int r = (wave * A_INS + i) * RPI + lrow;
+      a_src[i] = g.A + (size_t)min(tc.m0 + r, tc.m_end - 1) * g.K + (lphys ^ swz<BK>(r)) * 8;
+    }
+#pragma unroll
+    for (int i = 0; i < B_INS; ++i) {
+      const int r = (wave * B_INS + i) * RPI + lrow;
+      int brow;
+      if (GATED) brow = r < BN ? min(tc.n0 + r, g.N - 1) : g.up_row + min(tc.n0 + r - BN, g.N - 1);
+      else brow = min(tc.n0 + r, g.N - 1);
+      b_src[i] = Be + (size_t)brow * g.K + (lphys ^ swz<BK>(r)) * 8;
+    }
+  };
   auto issue = [&](int kt, int slot) {
     const int koff = kt * BK;
 #pragma unroll
@@ -271,57 +363,100 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
       __builtin_amdgcn_global_load_lds(MOEPD_GPTR(b_src[i] + koff),
                                        MOEPD_LPTR(&ring[slot][A_CH + (wave * B_INS + i) * 64]), 16, 0, 0);
   };
+  auto prologue = [&](const TileCoord& tc) {
+    set_sources(tc);
+#pragma unroll
+    for (int st = 0; st < STAGES; ++st)
+      if (st < KT) issue(st, st);
+  };
 
-  f32x16_t acc[FM][FN * NB];
+  bf16x8_t fa[2][FM], fb[2][FB];
+  auto read_frags = [&](int slot, int sub, bf16x8_t (&a)[FM], bf16x8_t (&b)[FB]) {
+    const u32x4* As = &ring[slot][0];
+    const u32x4* Bs = &ring[slot][A_CH];
+    const int ch = 2 * sub + (lane >> 5);
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+      const int r = wm * WTM + fm * 32 + (lane & 31);
+      a[fm] = as_bf16x8(As[r * CPR + (ch ^ swz<BK>(r))]);
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        const int r = nb * BN + wn * WTN + fn * 32 + (lane & 31);
+        b[nb * FN + fn] = as_bf16x8(Bs[r * CPR + (ch ^ swz<BK>(r))]);
+      }
+  };
+
+  f32x16_t acc[FM][FB];
+  auto mfmas = [&](const bf16x8_t (&a)[FM], const bf16x8_t (&b)[FB]) {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int j = 0; j < FB; ++j) acc[fm][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[fm], b[j], acc[fm][j], 0, 0, 0);
+  };
+
+  const int L = block_tile(g);
+  if (L < 0) return;
+  TileCoord tc;
+  tile_at(g, L, BM, BN, tc);
+  prologue(tc);
+
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN * NB; ++j)
+    for (int j = 0; j < FB; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  // 32-row blocks of this wave that hold rows of the expert (wave-uniform)
 
-  const int KT = g.K / BK;
-#pragma unroll
-  for (int st = 0; st < STAGES - 1; ++st)
-    if (st < KT) issue(st, st);
+  // slice 0 has landed once at most min(STAGES - 1, KT - 1) newer slices remain
+  wait_slices_lgkm0<NPS, STAGES - 1>(min(STAGES - 1, KT - 1));
+  bare_barrier();
+  read_frags(0, 0, fa[0], fb[0]);
 
-  int slot = 0;
-  for (int kt = 0; kt < KT; ++kt) {
-    // slice kt has landed once at most (newer slices issued) * NPS ops remain
-    wait_slices<NPS, STAGES - 2>(min(KT - 1 - kt, STAGES - 2));
-    bare_barrier();  // every wave's part of slice kt is in LDS; slot of kt-1 is free
-    if (kt + STAGES - 1 < KT) {
-      int ns = slot + STAGES - 1;
-      if (ns >= STAGES) ns -= STAGES;
-      issue(kt + STAGES - 1, ns);
-    }
-    const u32x4* As = &ring[slot][0];
-    const u32x4* Bs = &ring[slot][A_CH];
+  // One K slice.  MODE 0: slice kt + STAGES is issued into this slot after
+  // the barrier; MODE 1: no slices left to issue; MODE 2: the tile's last
+  // slice (no barrier, nothing to read ahead).  The three loops below keep
+  // each body straight-line code, so the accumulators stay in place.
+  auto slice = [&](auto mode, int kt, int slot) {
+    constexpr int MODE = decltype(mode)::value;
 #pragma unroll
-    for (int s = 0; s < BK / 16; ++s) {
-      const int ch = 2 * s + (lane >> 5);
-      bf16x8_t af[FM], bfr[FN * NB];
-#pragma unroll
-      for (int fm = 0; fm < FM; ++fm) {
-        const int r = wm * WTM + fm * 32 + (lane & 31);
-        af[fm] = as_bf16x8(As[r * CPR + (ch ^ swz<BK>(r))]);
+    for (int sub = 0; sub < SUB; ++sub) {
+      const int cur = sub & 1, nxt = cur ^ 1;
+      if (sub + 1 < SUB) {
+        read_frags(slot, sub + 1, fa[nxt], fb[nxt]);
+        mfmas(fa[cur], fb[cur]);
+        interleave<0, NMF, 0, NRD, 0>();
+      } else if constexpr (MODE < 2) {
+        // Every read of this slot is in registers once lgkmcnt is 0; slice
+        // kt + 1 has landed once at most min(STAGES - 2, KT - 2 - kt) newer
+        // slices remain.  After the barrier no wave reads this slot again,
+        // so slice kt + STAGES may overwrite it.
+        if constexpr (MODE == 0) wait_vmcnt_lgkm0<NPS * (STAGES - 2)>();
+        else wait_slices_lgkm0<NPS, STAGES - 2>(min(STAGES - 2, KT - 2 - kt));
+        bare_barrier();
+        int ns = slot + 1;
+        if (ns == STAGES) ns = 0;
+        if constexpr (MODE == 0) issue(kt + STAGES, slot);
+        read_frags(ns, 0, fa[nxt], fb[nxt]);
+        mfmas(fa[cur], fb[cur]);
+        interleave<0, NMF, MODE == 0 ? NPS : 0, NRD, 1>();
+      } else {
+        mfmas(fa[cur], fb[cur]);
       }
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int fn = 0; fn < FN; ++fn) {
-          const int r = nb * BN + wn * WTN + fn * 32 + (lane & 31);
-          bfr[nb * FN + fn] = as_bf16x8(Bs[r * CPR + (ch ^ swz<BK>(r))]);
-        }
-#pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-        for (int j = 0; j < FN * NB; ++j)
-          acc[fm][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[fm], bfr[j], acc[fm][j], 0, 0, 0);
     }
+  };
+  int kt = 0, slot = 0;
+  for (; kt < KT - STAGES; ++kt) {
+    slice(std::integral_constant<int, 0>{}, kt, slot);
     if (++slot == STAGES) slot = 0;
   }
+  for (; kt < KT - 1; ++kt) {
+    slice(std::integral_constant<int, 1>{}, kt, slot);
+    if (++slot == STAGES) slot = 0;
+  }
+  slice(std::integral_constant<int, 2>{}, kt, slot);
 
   // epilogue: SwiGLU -> bf16 h, or float32 y.  Rows are checked once per
   // 32-row block; only the expert's last block checks each row.
@@ -352,8 +487,10 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
 // Distinct entry points so that profiles name each GEMM of each regime.
 __global__ __launch_bounds__(256) void gemm1_swiglu_prefill(GemmArgs g) { gemm_ring_body<128, 256, 64, 2, 2, true, 3>(g); }
 __global__ __launch_bounds__(256) void gemm2_down_prefill(GemmArgs g) { gemm_ring_body<128, 256, 64, 2, 2, false, 3>(g); }
-__global__ __launch_bounds__(256) void gemm1_swiglu_decode(GemmArgs g) { gemm_skinny<true>(g); }
-__global__ __launch_bounds__(256) void gemm2_down_decode(GemmArgs g) { gemm_skinny<false>(g); }
+template <bool ROT>
+__global__ __launch_bounds__(256) void gemm1_swiglu_decode(GemmArgs g) { gemm_skinny<true, ROT>(g); }
+template <bool ROT>
+__global__ __launch_bounds__(256) void gemm2_down_decode(GemmArgs g) { gemm_skinny<false, ROT>(g); }
 
 // ------------------------------------------------------------------ launch
 
@@ -392,8 +529,14 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
   } else {
     g.n_tiles = (g.N + 127) / 128;
     const dim3 grid(round8((long long)max_m_tiles * g.n_tiles));
-    if (gemm == 1) gemm1_swiglu_decode<<<grid, 256, 0, s>>>(g);
-    else gemm2_down_decode<<<grid, 256, 0, s>>>(g);
+    const bool rot = g.K % 2048 == 0;
+    if (gemm == 1) {
+      if (rot) gemm1_swiglu_decode<true><<<grid, 256, 0, s>>>(g);
+      else gemm1_swiglu_decode<false><<<grid, 256, 0, s>>>(g);
+    } else {
+      if (rot) gemm2_down_decode<true><<<grid, 256, 0, s>>>(g);
+      else gemm2_down_decode<false><<<grid, 256, 0, s>>>(g);
+    }
   }
   return hipGetLastError();
 }

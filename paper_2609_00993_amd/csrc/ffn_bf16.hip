@@ -186,6 +186,10 @@ __device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
   gemm_skinny_tile<GATED, ROT>(g, tc);
 }
 
+// Word 3 of a raw (unstructured) buffer resource on gfx9: 32-bit data
+// format, no swizzle; out-of-range loads return zero without a memory access.
+constexpr int kBufferRsrcWord3 = 0x00020000;
+
 #define MOEPD_GPTR(p) ((const void __attribute__((address_space(1)))*)(p))
 #define MOEPD_LPTR(p) ((void __attribute__((address_space(3)))*)(p))
 
@@ -334,14 +338,23 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   // chunk (l % CPR) ^ swz(r).
   const int lrow = lane / CPR, lphys = lane % CPR;
 
-  const uint16_t* a_src[A_INS];
+  // A rows are read through a buffer resource that covers exactly the
+  // tile's rows of its expert: rows past the expert's end fall outside it,
+  // so their loads return zeros and make no memory request (the output rows
+  // they feed are never stored).  B rows past N are clamped to the last.
+  __amdgpu_buffer_rsrc_t a_rsrc;
+  uint32_t a_off[A_INS];  // byte offset of each A instruction's row chunk
   const uint16_t* b_src[B_INS];
   auto set_sources = [&](const TileCoord& tc) {
-    const uint16_t* Be = g.B + (size_t)tc.e * g.b_stride;
+    const int m0 = __builtin_amdgcn_readfirstlane(tc.m0);
+    const int rows = min(__builtin_amdgcn_readfirstlane(tc.m_end) - m0, BM);
+    a_rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(g.A + (size_t)m0 * g.K), (short)0, rows * g.K * 2,
+                                               kBufferRsrcWord3);
+    const uint16_t* Be = g.B + (size_t)__builtin_amdgcn_readfirstlane(tc.e) * g.b_stride;
 #pragma unroll
     for (int i = 0; i < A_INS; ++i) {
       const int r = (wave * A_INS + i) * RPI + lrow;
-      a_src[i] = g.A + (size_t)min(tc.m0 + r, tc.m_end - 1) * g.K + (lphys ^ swz<BK>(r)) * 8;
+      a_off[i] = (uint32_t)(r * g.K + (lphys ^ swz<BK>(r)) * 8) * 2u;
     }
 #pragma unroll
     for (int i = 0; i < B_INS; ++i) {
@@ -356,8 +369,8 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
     const int koff = kt * BK;
 #pragma unroll
     for (int i = 0; i < A_INS; ++i)
-      __builtin_amdgcn_global_load_lds(MOEPD_GPTR(a_src[i] + koff), MOEPD_LPTR(&ring[slot][(wave * A_INS + i) * 64]),
-                                       16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, MOEPD_LPTR(&ring[slot][(wave * A_INS + i) * 64]), 16,
+                                               a_off[i] + (uint32_t)koff * 2u, 0, 0, 0);
 #pragma unroll
     for (int i = 0; i < B_INS; ++i)
       __builtin_amdgcn_global_load_lds(MOEPD_GPTR(b_src[i] + koff),

@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--d-iters", type=int, default=60, help="D layers per latency measurement")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--d-priority-us", type=int, default=100,
+                    help="D-first admission: longest wait of a P GEMM tile for an in-flight D layer (0 = off)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="instead of the layer, time a plain device copy of this many MiB (the reference kernel "
                          "for scaling the HBM byte counters)")
@@ -201,7 +203,8 @@ def main():
     T = {0: spec.T_P, 1: spec.T_D}
     outs = {ph: torch.empty((T[ph], spec.H), dtype=torch.float32, device=dev) for ph in (0, 1)}
     cfg = M.make_config(spec.E, spec.e0, spec.E_loc, spec.k, spec.H, spec.I,
-                        M.MOE_DTYPE_BF16 if bf16 else M.MOE_DTYPE_F32, T[0], T[1])
+                        M.MOE_DTYPE_BF16 if bf16 else M.MOE_DTYPE_F32, T[0], T[1],
+                        d_priority_us=args.d_priority_us)
     st, ctx = M.moe_ctx_create(cfg, w_gu, w_dn)
     M.check(st, "moe_ctx_create")
     sP, sD = torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev)
@@ -344,7 +347,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": workload_name(spec), "E": spec.E, "E_loc": spec.E_loc, "top_k": spec.k, "H": spec.H,
                    "I": spec.I, "T_P": spec.T_P, "T_D": spec.T_D, "rows_P": rows[0], "rows_D": rows[1],
-                   "parallelism": "single GPU, P and D on two streams"},
+                   "parallelism": "single GPU, P and D on two streams", "d_priority_us": args.d_priority_us},
         "d_latency_us": {
             "p50_alone": round(p50a, 2), "p90_alone": round(pct(lat_alone, 90), 2),
             "p50_under_p": round(p50u, 2), "p90_under_p": round(pct(lat_under, 90), 2),

@@ -111,6 +111,14 @@ typedef struct moe_config {
   int32_t dtype;             /* MOE_DTYPE_F32 or MOE_DTYPE_BF16 */
   int32_t max_tokens[MOE_NUM_PHASES]; /* capacity per phase, 0..1048576 */
   int32_t flags;             /* must be 0 */
+  /* D-first admission, 0..1000 (0 = off).  Section 3.1: ready D work is
+   * admitted before P, and a long P execution is cut into segments so that D
+   * advances between them (Section 4.2).  On one GPU a P segment is one tile
+   * of its grouped GEMMs: while a D layer is in flight (from the start of its
+   * moe_route kernel to the start of its moe_combine kernel), a P grouped-GEMM
+   * workgroup about to start a tile waits for the D layer, for at most about
+   * this many microseconds.  A scheduling hint only: results are unchanged. */
+  int32_t d_priority_us;
 } moe_config_t;
 
 /* Borrowed, read-only expert weights for the E_loc resident experts, shared by

@@ -19,7 +19,10 @@ constexpr int kCombVec = 4;  // 16-byte vectors per lane per pass
 
 __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ y, const float* __restrict__ topk_w,
                                                       const int32_t* __restrict__ row_of_slot, int T, int k, int nv,
-                                                      u32x4* __restrict__ out) {
+                                                      u32x4* __restrict__ out, WindowSignal close) {
+  // The layer's grouped GEMMs are done once this kernel runs: close the window.
+  if (close.word && blockIdx.x == 0 && threadIdx.x == 0)
+    __hip_atomic_store(close.word, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;  // whole wave leaves together
   const int lane = threadIdx.x & 63;
@@ -65,11 +68,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ 
 }
 
 hipError_t launch_combine(const void* y, const float* topk_w, const int32_t* row_of_slot, int T, int k, int H,
-                          void* out, hipStream_t s) {
+                          void* out, WindowSignal close, hipStream_t s) {
   if (T <= 0) return hipSuccess;
   const int nv = H * 4 / 16;
   combine_kernel<<<dim3((T + 3) / 4), dim3(256), 0, s>>>((const u32x4*)y, topk_w, row_of_slot, T, k, nv,
-                                                          (u32x4*)out);
+                                                          (u32x4*)out, close);
   return hipGetLastError();
 }
 

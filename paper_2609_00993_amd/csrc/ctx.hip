@@ -46,6 +46,10 @@ struct Phase {
   hipEvent_t ev = nullptr;
   bool ev_recorded = false;
   hipStream_t last_stream = nullptr;
+  // Generation stored in the signal word while this phase's layer window is
+  // open.  A reset moves to a new generation, so a window left open by an
+  // abandoned layer is no longer honoured.
+  int32_t gen = 1;
   Timing timing[MOE_NUM_KERNELS];
 };
 
@@ -72,6 +76,7 @@ bool valid_config(const moe_config_t* c) {
   for (int p = 0; p < MOE_NUM_PHASES; ++p)
     if (c->max_tokens[p] < 0 || c->max_tokens[p] > (1 << 20)) return false;
   if (c->flags != 0) return false;
+  if (c->d_priority_us < 0 || c->d_priority_us > 1000) return false;
   return true;
 }
 
@@ -131,7 +136,7 @@ int alloc_phase(moe_ctx* ctx, int phase) {
   const size_t o_ros = take(slots * 4), o_tor = take(p.rows_cap * 4);
   const size_t o_xp = take(p.rows_cap * c.hidden * ctx->esz), o_h = take(p.rows_cap * c.inter * ctx->esz);
   const size_t o_y = take(p.rows_cap * c.hidden * 4);
-  const size_t o_cc = take((size_t)E * mc * 4), o_tb = take((E + 1) * 4);
+  const size_t o_cc = take((size_t)E * mc * 4), o_tb = take((E + 1) * 4), o_sig = take(4);
 
   void* mem = nullptr;
   if (hipMalloc(&mem, off) != hipSuccess || !mem) {
@@ -151,7 +156,9 @@ int alloc_phase(moe_ctx* ctx, int phase) {
   p.b.y = (float*)(base + o_y);
   p.b.chunk_counts = (int32_t*)(base + o_cc);
   p.b.tile_base = (int32_t*)(base + o_tb);
-  // Zero the small metadata (counts, offsets, tile prefix) once at creation.
+  p.b.signal = (int32_t*)(base + o_sig);
+  // Zero the small metadata (counts, offsets, tile prefix, signal word) once
+  // at creation.
   if (hipMemset(base + o_cnt, 0, o_ros - o_cnt) != hipSuccess) return MOE_ERR_HIP;
   if (hipMemset(base + o_tb, 0, off - o_tb) != hipSuccess) return MOE_ERR_HIP;
   if (hipEventCreateWithFlags(&p.ev, hipEventDisableTiming) != hipSuccess) {
@@ -197,6 +204,20 @@ int timed(Phase& p, int kernel, hipStream_t s, F&& launch) {
   return MOE_OK;
 }
 
+// The D phase announces its layer window when D-first admission is on.
+WindowSignal window_of(moe_ctx* ctx, int phase) {
+  if (phase != MOE_PHASE_D || ctx->cfg.d_priority_us <= 0) return WindowSignal{nullptr, 0};
+  Phase& p = ctx->ph[phase];
+  return WindowSignal{p.b.signal, p.gen};
+}
+
+// The P phase's grouped GEMMs hold back while the D window is open; one poll
+// sleeps 127 * 64 cycles, about 3.4 us at 2.4 GHz.
+YieldTo yield_of(moe_ctx* ctx, int phase) {
+  if (phase != MOE_PHASE_P || ctx->cfg.d_priority_us <= 0) return YieldTo{nullptr, 0, 0};
+  const Phase& d = ctx->ph[MOE_PHASE_D];
+  return YieldTo{d.b.signal, d.gen, (ctx->cfg.d_priority_us * 10 + 33) / 34};
+}
 }  // namespace
 
 extern "C" {
@@ -238,7 +259,10 @@ int moe_route(moe_ctx_t* ctx, int phase, const float* logits, int32_t T, hipStre
   const moe_config_t& c = ctx->cfg;
   if (T > 0) {
     st = timed(p, MOE_KERNEL_ROUTE, stream,
-               [&] { return launch_route(logits, T, c.num_experts, c.top_k, p.b.topk_idx, p.b.topk_w, stream); });
+               [&] {
+                 return launch_route(logits, T, c.num_experts, c.top_k, p.b.topk_idx, p.b.topk_w,
+                                     window_of(ctx, phase), stream);
+               });
     if (st) return st;
   }
   if ((st = leave(p, stream))) return st;
@@ -302,7 +326,7 @@ int moe_expert_ffn(moe_ctx_t* ctx, int phase, hipStream_t stream) {
       st = timed(p, gemm == 1 ? MOE_KERNEL_GEMM1 : MOE_KERNEL_GEMM2, stream, [&] {
         if (c.dtype == MOE_DTYPE_BF16)
           return launch_ffn_bf16(p.regime, gemm, p.b, ctx->w.w_gate_up, ctx->w.w_down, c.num_local_experts, c.hidden,
-                                 c.inter, max_m_tiles, stream);
+                                 c.inter, max_m_tiles, yield_of(ctx, phase), stream);
         return launch_ffn_f32(gemm, p.b, ctx->w.w_gate_up, ctx->w.w_down, c.num_local_experts, c.hidden, c.inter,
                               max_m_tiles, stream);
       });
@@ -325,7 +349,8 @@ int moe_combine(moe_ctx_t* ctx, int phase, void* out, hipStream_t stream) {
   const moe_config_t& c = ctx->cfg;
   if (p.T > 0) {
     st = timed(p, MOE_KERNEL_COMBINE, stream, [&] {
-      return launch_combine(p.b.y, p.b.topk_w, p.b.row_of_slot, p.T, c.top_k, c.hidden, out, stream);
+      return launch_combine(p.b.y, p.b.topk_w, p.b.row_of_slot, p.T, c.top_k, c.hidden, out, window_of(ctx, phase),
+                            stream);
     });
     if (st) return st;
   }
@@ -367,6 +392,7 @@ int moe_phase_reset(moe_ctx_t* ctx, int phase) {
   }
   p.state = MOE_STATE_IDLE;
   p.T = 0;
+  p.gen = p.gen == 0x3fffffff ? 1 : p.gen + 1;
   return MOE_OK;
 }
 

@@ -44,6 +44,7 @@ struct GemmArgs {
   const int32_t* tile_base;
   long long b_stride;
   int e_loc, N, K, n_tiles, up_row;
+  YieldTo yield;  // the other phase's layer window to hold back for, if any
 };
 
 struct TileCoord {
@@ -91,6 +92,21 @@ __device__ __forceinline__ int block_tile(const GemmArgs& g) {
 // for them.
 __device__ __forceinline__ int k_rotation(const TileCoord& tc, int n_tiles, int bn, int nk) {
   return (int)((unsigned)((tc.e * n_tiles + tc.n0 / bn) * 2) % (unsigned)nk);
+}
+
+// D first (Section 3.1): the planner admits ready D work before P, and a
+// long P execution is cut into segments so that D advances between them
+// (Section 4.2).  On one GPU the segment is a GEMM tile: while the other
+// phase's layer window is open, a workgroup about to start a tile sleeps in
+// steps of 127 * 64 cycles until the window closes, at most `polls` times.
+// The wait is bounded, so the kernel always finishes, and it is only a hint:
+// no result depends on it.
+__device__ __forceinline__ void yield_to_window(const YieldTo& y) {
+  if (!y.word) return;
+  for (int i = 0; i < y.polls; ++i) {
+    if (__hip_atomic_load(y.word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != y.gen) return;
+    __builtin_amdgcn_s_sleep(127);
+  }
 }
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const u32x4& u) { return __builtin_bit_cast(bf16x8_t, u); }
@@ -181,6 +197,7 @@ __device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
   constexpr int BM = 32, BN = 128;
   const int L = block_tile(g);
   if (L < 0) return;
+  yield_to_window(g.yield);
   TileCoord tc;
   tile_at(g, L, BM, BN, tc);
   gemm_skinny_tile<GATED, ROT>(g, tc);
@@ -412,6 +429,7 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
 
   const int L = block_tile(g);
   if (L < 0) return;
+  yield_to_window(g.yield);
   TileCoord tc;
   tile_at(g, L, BM, BN, tc);
   prologue(tc);
@@ -512,8 +530,9 @@ int ffn_bf16_bm(int regime) { return regime == 0 ? 128 : 32; }
 static inline int round8(long long v) { return (int)((v + 7) / 8 * 8); }
 
 hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
-                           int e_loc, int H, int I, int max_m_tiles, hipStream_t s) {
+                           int e_loc, int H, int I, int max_m_tiles, YieldTo yield, hipStream_t s) {
   GemmArgs g;
+  g.yield = yield;
   g.offsets = b.offsets;
   g.tile_base = b.tile_base;
   g.e_loc = e_loc;

@@ -22,6 +22,25 @@ struct PhaseBuffers {
   // workspace
   int32_t* chunk_counts;  // [E_loc * max_chunks], expert-major
   int32_t* tile_base;     // [E_loc + 1], prefix sum of m-tiles per expert
+  // Signal word of this phase's layer window: a generation number while a
+  // layer is between its route and its combine, 0 otherwise.  Written only
+  // by this phase's kernels; read by the other phase's grouped GEMMs.
+  int32_t* signal;
+};
+
+// A layer window announced to the other phase: the kernels that open and
+// close it store `gen` / 0 into `word` (null: no window).
+struct WindowSignal {
+  int32_t* word;
+  int32_t gen;
+};
+
+// A window to yield to: a grouped-GEMM workgroup of the other phase waits
+// while *word == gen, at most `polls` sleeps of about 3.4 us (null: never).
+struct YieldTo {
+  const int32_t* word;
+  int32_t gen;
+  int32_t polls;
 };
 
 // Largest number of (expert, chunk) histogram cells the count kernel scans.
@@ -39,7 +58,7 @@ inline int dispatch_chunk_tokens(int T, int k, int e_loc) {
 }
 
 hipError_t launch_route(const float* logits, int T, int E, int k, int32_t* topk_idx, float* topk_w,
-                        hipStream_t s);
+                        WindowSignal open, hipStream_t s);
 
 // Histogram of each chunk's slots per local expert -> chunk_counts.
 hipError_t launch_count(const int32_t* topk_idx, int T, int k, int e0, int e_loc, int chunk_tokens, int nchunks,
@@ -57,14 +76,14 @@ hipError_t launch_permute(const void* x, int T, int k, int row_bytes, const int3
 
 // out[t] = sum_j w[t,j] y[row(t,j)] in float32 (y and out are float32).
 hipError_t launch_combine(const void* y, const float* topk_w, const int32_t* row_of_slot, int T, int k, int H,
-                          void* out, hipStream_t s);
+                          void* out, WindowSignal close, hipStream_t s);
 
 // Grouped expert FFN.  `regime` picks the tile configuration (0 = large
 // batches, 1 = small batches); bm_of_regime gives its m-tile height, which
 // the count kernel must use for tile_base.
 int ffn_bf16_bm(int regime);
 hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
-                           int e_loc, int H, int I, int max_m_tiles, hipStream_t s);
+                           int e_loc, int H, int I, int max_m_tiles, YieldTo yield, hipStream_t s);
 
 int ffn_f32_bm();
 hipError_t launch_ffn_f32(int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn, int e_loc, int H,

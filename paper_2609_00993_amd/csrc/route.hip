@@ -32,7 +32,10 @@ __device__ __forceinline__ float from_orderable(uint32_t o) {
 
 template <int EPL>
 __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ logits, int T, int E, int k,
-                                                    int32_t* __restrict__ topk_idx, float* __restrict__ topk_w) {
+                                                    int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
+                                                    WindowSignal open) {
+  if (open.word && blockIdx.x == 0 && threadIdx.x == 0)
+    __hip_atomic_store(open.word, open.gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const int lane = lane_id();
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;  // whole wave leaves together
@@ -73,19 +76,20 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
   }
 }
 
-hipError_t launch_route(const float* logits, int T, int E, int k, int32_t* topk_idx, float* topk_w, hipStream_t s) {
+hipError_t launch_route(const float* logits, int T, int E, int k, int32_t* topk_idx, float* topk_w,
+                        WindowSignal open, hipStream_t s) {
   if (T <= 0) return hipSuccess;
   const dim3 grid((T + 3) / 4), block(256);
   if (E <= 64)
-    route_kernel<1><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w);
+    route_kernel<1><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open);
   else if (E <= 128)
-    route_kernel<2><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w);
+    route_kernel<2><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open);
   else if (E <= 256)
-    route_kernel<4><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w);
+    route_kernel<4><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open);
   else if (E <= 512)
-    route_kernel<8><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w);
+    route_kernel<8><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open);
   else
-    route_kernel<16><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w);
+    route_kernel<16><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open);
   return hipGetLastError();
 }
 

@@ -56,6 +56,7 @@ class moe_config_t(ctypes.Structure):
         ("dtype", c_int32),
         ("max_tokens", c_int32 * 2),
         ("flags", c_int32),
+        ("d_priority_us", c_int32),
     ]
 
 
@@ -142,7 +143,7 @@ def _stream(s) -> int:
 
 
 def make_config(num_experts, expert_begin, num_local_experts, top_k, hidden, inter, dtype, max_tokens_p,
-                max_tokens_d, flags=0) -> moe_config_t:
+                max_tokens_d, flags=0, d_priority_us=0) -> moe_config_t:
     c = moe_config_t()
     c.num_experts = num_experts
     c.expert_begin = expert_begin
@@ -154,6 +155,7 @@ def make_config(num_experts, expert_begin, num_local_experts, top_k, hidden, int
     c.max_tokens[0] = max_tokens_p
     c.max_tokens[1] = max_tokens_d
     c.flags = flags
+    c.d_priority_us = d_priority_us
     return c
 
 

@@ -46,7 +46,7 @@ def to_dev(a: np.ndarray):
 class GpuLayer:
     """One context over a LayerInputs, with per-phase streams and outputs."""
 
-    def __init__(self, inp, max_tokens=None):
+    def __init__(self, inp, max_tokens=None, d_priority_us=0):
         import torch
 
         from paper_2609_00993_amd import moepd as M
@@ -65,7 +65,8 @@ class GpuLayer:
         self.logits = {ph: to_dev(inp.logits[ph]) for ph in (0, 1)}
         self.out = {ph: torch.zeros((self.T[ph], spec.H), dtype=torch.float32, device="cuda") for ph in (0, 1)}
         cfg = M.make_config(spec.E, spec.e0, spec.E_loc, spec.k, spec.H, spec.I,
-                            M.MOE_DTYPE_BF16 if self.bf16 else M.MOE_DTYPE_F32, max_tokens[0], max_tokens[1])
+                            M.MOE_DTYPE_BF16 if self.bf16 else M.MOE_DTYPE_F32, max_tokens[0], max_tokens[1],
+                            d_priority_us=d_priority_us)
         st, self.ctx = M.moe_ctx_create(cfg, self.w_gu, self.w_dn)
         M.check(st, "moe_ctx_create")
         self.streams = {0: torch.cuda.Stream(), 1: torch.cuda.Stream()}

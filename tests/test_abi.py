@@ -63,7 +63,7 @@ def _cfg(lib, **kw):
     dict(expert_begin=-1), dict(expert_begin=4), dict(top_k=0), dict(top_k=9), dict(top_k=17, num_experts=32,
                                                                                   num_local_experts=32),
     dict(hidden=100), dict(hidden=32), dict(inter=96), dict(dtype=7), dict(max_tokens_p=-1),
-    dict(max_tokens_d=(1 << 20) + 1), dict(flags=1),
+    dict(max_tokens_d=(1 << 20) + 1), dict(flags=1), dict(d_priority_us=-1), dict(d_priority_us=1001),
 ])
 def test_create_rejects_bad_config_without_gpu(lib, bad):
     st, ctx = lib.moe_ctx_create(_cfg(lib, **bad), 0x1000, 0x2000)

@@ -83,13 +83,15 @@ def _snapshot(g, ph):
     return {k: v.copy() for k, v in res.items() if isinstance(v, np.ndarray)}
 
 
-def test_concurrent_phases_bit_identical_to_solo():
+@pytest.mark.parametrize("d_priority_us", [0, 200])
+def test_concurrent_phases_bit_identical_to_solo(d_priority_us):
     """P and D enqueued on two streams at once give the same bits as each
-    phase run alone: the phases share only read-only weights."""
+    phase run alone: the phases share only read-only weights, and D-first
+    admission only delays P's tiles."""
     import torch
 
     inp = make_config(1)
-    g = GpuLayer(inp)
+    g = GpuLayer(inp, d_priority_us=d_priority_us)
     try:
         g.run(0)
         p_solo = _snapshot(g, 0)
@@ -105,6 +107,40 @@ def test_concurrent_phases_bit_identical_to_solo():
                 assert np.array_equal(d[key], d_solo[key]), (rep, "D", key)
         check_phase(g, inp, 0)
         check_phase(g, inp, 1)
+    finally:
+        g.close()
+
+
+def test_abandoned_d_window_is_not_honoured():
+    """A D layer abandoned after its route leaves its window open on the
+    device; after moe_phase_reset the P phase no longer waits for it (the
+    reset moves D to a new window generation).  P still gives the oracle's
+    result, and well inside the time a wait on every tile would take."""
+    import time
+
+    import torch
+
+    inp = make_config(1)
+    g = GpuLayer(inp, d_priority_us=1000)
+    try:
+        M = g.M
+        g.run(0)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        g.run(0)
+        torch.cuda.synchronize()
+        base = time.perf_counter() - t0
+        s = g.streams[1]
+        M.check(M.moe_route(g.ctx, 1, g.logits[1], g.T[1], s))
+        torch.cuda.synchronize()
+        M.check(M.moe_phase_reset(g.ctx, 1))
+        t0 = time.perf_counter()
+        g.run(0)
+        torch.cuda.synchronize()
+        after = time.perf_counter() - t0
+        # a wait on every tile would add at least 1 ms per round of tiles
+        assert after < base + 2e-3, (base, after)
+        check_phase(g, inp, 0)
     finally:
         g.close()
 

@@ -17,7 +17,11 @@ JSON line with:
   peak that bounds it.  Durations come from HIP events recorded around every
   kernel on the stream it runs on, over a second pass of the same K timed
   steps (the events themselves cost stream time, so the throughput pass runs
-  without them);
+  without them) with D-first admission off, so that a P kernel's duration is
+  its own work and not the waits the admission policy puts in it;
+* D-first admission (--d-priority-us, default 100): while a D layer is in
+  flight, P grouped-GEMM tiles wait for it, up to that bound; value and
+  d_latency_us are measured with it, without_d_first repeats both without;
 * kernels: mean launch duration of every kernel of both phases;
 * cpu_baseline: the CPU oracle timed on a bounded sample on this host.
 """
@@ -202,51 +206,58 @@ def main():
     lg = {ph: up(inp.logits[ph]) for ph in (0, 1)}
     T = {0: spec.T_P, 1: spec.T_D}
     outs = {ph: torch.empty((T[ph], spec.H), dtype=torch.float32, device=dev) for ph in (0, 1)}
-    cfg = M.make_config(spec.E, spec.e0, spec.E_loc, spec.k, spec.H, spec.I,
-                        M.MOE_DTYPE_BF16 if bf16 else M.MOE_DTYPE_F32, T[0], T[1],
-                        d_priority_us=args.d_priority_us)
-    st, ctx = M.moe_ctx_create(cfg, w_gu, w_dn)
-    M.check(st, "moe_ctx_create")
+    def make_ctx(d_priority_us):
+        cfg = M.make_config(spec.E, spec.e0, spec.E_loc, spec.k, spec.H, spec.I,
+                            M.MOE_DTYPE_BF16 if bf16 else M.MOE_DTYPE_F32, T[0], T[1], d_priority_us=d_priority_us)
+        st, c = M.moe_ctx_create(cfg, w_gu, w_dn)
+        M.check(st, "moe_ctx_create")
+        return c
+
+    # The bench line runs at the D-first admission bound given (ctx); the same
+    # layer without it (ctx_off) gives the comparison figures and the
+    # per-kernel durations, which must not include P's deliberate waits.
+    ctx = make_ctx(args.d_priority_us)
+    ctx_off = make_ctx(0) if args.d_priority_us > 0 else ctx
     sP, sD = torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev)
     streams = {0: sP, 1: sD}
 
-    def layer(ph):
-        M.layer(ctx, ph, lg[ph], T[ph], xs[ph], outs[ph], streams[ph])
+    def layer(ph, c=None):
+        M.layer(ctx if c is None else c, ph, lg[ph], T[ph], xs[ph], outs[ph], streams[ph])
 
     # ---- warmup
-    for _ in range(max(1, args.warmup)):
-        layer(0)
-        layer(1)
+    for c in {ctx, ctx_off}:
+        for _ in range(max(1, args.warmup)):
+            layer(0, c)
+            layer(1, c)
     torch.cuda.synchronize()
 
     # ---- timed concurrent steps: throughput (no per-kernel events, which
     # would add a stream command around every kernel)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        layer(0)
-        layer(1)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    def timed_steps(c):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            layer(0, c)
+            layer(1, c)
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
+    wall = timed_steps(ctx)
+    wall_off = timed_steps(ctx_off) if ctx_off is not ctx else wall
 
     # ---- the same K concurrent steps again with per-kernel HIP events on the
-    # launching streams: per-kernel durations for the roofline
-    M.check(M.moe_timing_enable(ctx, args.steps), "moe_timing_enable")
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    for _ in range(args.steps):
-        layer(0)
-        layer(1)
-    torch.cuda.synchronize()
-    wall_events = time.perf_counter() - t1
+    # launching streams (D-first admission off): per-kernel durations for the
+    # roofline
+    M.check(M.moe_timing_enable(ctx_off, args.steps), "moe_timing_enable")
+    wall_events = timed_steps(ctx_off)
     kern = {}
     for ph in (0, 1):
         for kid in range(M.MOE_NUM_KERNELS):
-            st, ms, n = M.moe_timing_read(ctx, ph, kid)
+            st, ms, n = M.moe_timing_read(ctx_off, ph, kid)
             M.check(st)
             if n:
                 kern[(ph, M.moe_kernel_name(kid))] = (ms, n)
-    M.check(M.moe_timing_enable(ctx, 0))
+    M.check(M.moe_timing_enable(ctx_off, 0))
 
     # rows and touched experts of each phase (device-side layout, read once)
     rows, touched = {}, {}
@@ -263,7 +274,7 @@ def main():
         touched[ph] = int((counts > 0).sum())
 
     # ---- D latency alone and under P
-    def d_latencies(under_p):
+    def d_latencies(under_p, c):
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in
                range(args.d_iters)]
         p_first = torch.cuda.Event(enable_timing=True)
@@ -273,14 +284,14 @@ def main():
             p_first.record(sP)
             n_p = 4
             for _ in range(n_p):
-                layer(0)
+                layer(0, c)
         lat = []
         for i in range(args.d_iters):
             a, b = evs[i]
             if under_p:
-                layer(0)  # keep the P stream one layer ahead
+                layer(0, c)  # keep the P stream one layer ahead
             a.record(sD)
-            layer(1)
+            layer(1, c)
             b.record(sD)
             if not under_p:
                 sD.synchronize()
@@ -293,8 +304,13 @@ def main():
             overlapped = sum(1 for a, b in evs if p_first.elapsed_time(a) >= 0 and b.elapsed_time(p_last) >= 0)
         return lat, overlapped
 
-    lat_alone, _ = d_latencies(False)
-    lat_under, overlapped = d_latencies(True)
+    lat_alone, _ = d_latencies(False, ctx)
+    lat_under, overlapped = d_latencies(True, ctx)
+    if ctx_off is not ctx:
+        lat_alone_off, _ = d_latencies(False, ctx_off)
+        lat_under_off, _ = d_latencies(True, ctx_off)
+    else:
+        lat_alone_off, lat_under_off = lat_alone, lat_under
 
     # ---- roofline of the dominant kernel
     tot = {}
@@ -357,8 +373,19 @@ def main():
         "roofline": roof,
         "kernels": kernels,
         "kernels_pass_ms_per_step": round(wall_events / args.steps * 1e3, 4),
+        "kernels_pass_note": "per-kernel HIP events over a second pass of the same concurrent steps, D-first admission "
+                             "off, so P kernel durations hold no deliberate waits",
+        "without_d_first": {
+            "value": round((T[0] + T[1]) * args.steps / wall_off, 1),
+            "ms_per_step": round(wall_off / args.steps * 1e3, 4),
+            "d_p50_alone_us": round(pct(lat_alone_off, 50), 2),
+            "d_p50_under_p_us": round(pct(lat_under_off, 50), 2),
+            "ratio_p50": round(pct(lat_under_off, 50) / pct(lat_alone_off, 50), 3),
+        },
     }
     M.check(M.moe_ctx_destroy(ctx))
+    if ctx_off is not ctx:
+        M.check(M.moe_ctx_destroy(ctx_off))
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
     print(json.dumps(res), flush=True)

@@ -283,9 +283,12 @@ int moe_dispatch(moe_ctx_t* ctx, int phase, const void* x, hipStream_t stream) {
   const int T = p.T, k = c.top_k, E_loc = c.num_local_experts;
   chunking(T, k, E_loc, &p.chunk_tokens, &p.nchunks);
   if (c.dtype == MOE_DTYPE_BF16) {
-    // Rows per resident expert expected under even routing: T*k/E.
+    // Rows per resident expert expected under even routing: T*k/E.  Small
+    // batches stream weights (32-row tiles); large ones take 128-row tiles,
+    // and very large ones 256-row tiles, which move a third fewer bytes into
+    // LDS per flop.
     const long long avg = (long long)T * k / c.num_experts;
-    p.regime = avg >= 32 ? 0 : 1;
+    p.regime = avg >= 512 ? 2 : avg >= 32 ? 0 : 1;
     p.bm = ffn_bf16_bm(p.regime);
   } else {
     p.regime = 0;

@@ -44,6 +44,7 @@ struct GemmArgs {
   const int32_t* tile_base;
   long long b_stride;
   int e_loc, N, K, n_tiles, up_row;
+  int n_group;  // n-tiles per block of the within-expert tile order (see tile_at)
   YieldTo yield;  // the other phase's layer window to hold back for, if any
 };
 
@@ -51,7 +52,12 @@ struct TileCoord {
   int e, m0, m_end, n0;
 };
 
-// Coordinates of logical tile L (expert-major, then n-tile, then m-tile).
+// Coordinates of logical tile L.  Tiles run expert-major.  Within an expert
+// (mt m-tiles x n_tiles n-tiles) the n-tiles are cut into blocks of n_group;
+// block by block, the tiles go m-tile by m-tile, n-tile fastest.  So
+// consecutive tiles (which one XCD runs side by side, see block_tile) share
+// an activation row block across n_group n-tiles and a weight n-tile across
+// the m-tiles running together.  n_group = n_tiles is plain m-major order.
 __device__ __forceinline__ void tile_at(const GemmArgs& g, int L, int bm, int bn, TileCoord& tc) {
   int lo = 0, hi = g.e_loc - 1;
   while (lo < hi) {
@@ -62,7 +68,15 @@ __device__ __forceinline__ void tile_at(const GemmArgs& g, int L, int bm, int bn
   const int e = lo;
   const int mt_e = g.tile_base[e + 1] - g.tile_base[e];
   const int local = L - g.tile_base[e] * g.n_tiles;
-  const int nt = local / mt_e, mt = local - nt * mt_e;
+  const int b = g.n_group;
+  const int full = g.n_tiles / b;  // full n-blocks; a narrower one may follow
+  int blk = local / (mt_e * b), bw = b, r;
+  if (blk >= full) {
+    blk = full;
+    bw = g.n_tiles - full * b;
+  }
+  r = local - blk * mt_e * b;
+  const int mt = r / bw, nt = blk * b + (r - mt * bw);
   tc.e = e;
   tc.m0 = g.offsets[e] + mt * bm;
   tc.m_end = g.offsets[e + 1];
@@ -518,6 +532,8 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
 // Distinct entry points so that profiles name each GEMM of each regime.
 __global__ __launch_bounds__(256) void gemm1_swiglu_prefill(GemmArgs g) { gemm_ring_body<128, 256, 64, 2, 2, true, 3>(g); }
 __global__ __launch_bounds__(256) void gemm2_down_prefill(GemmArgs g) { gemm_ring_body<128, 256, 64, 2, 2, false, 3>(g); }
+__global__ __launch_bounds__(256) void gemm1_swiglu_wide(GemmArgs g) { gemm_ring_body<256, 256, 32, 2, 2, true, 4>(g); }
+__global__ __launch_bounds__(256) void gemm2_down_wide(GemmArgs g) { gemm_ring_body<256, 256, 32, 2, 2, false, 4>(g); }
 template <bool ROT>
 __global__ __launch_bounds__(256) void gemm1_swiglu_decode(GemmArgs g) { gemm_skinny<true, ROT>(g); }
 template <bool ROT>
@@ -525,7 +541,7 @@ __global__ __launch_bounds__(256) void gemm2_down_decode(GemmArgs g) { gemm_skin
 
 // ------------------------------------------------------------------ launch
 
-int ffn_bf16_bm(int regime) { return regime == 0 ? 128 : 32; }
+int ffn_bf16_bm(int regime) { return regime == 0 ? 128 : regime == 2 ? 256 : 32; }
 
 static inline int round8(long long v) { return (int)((v + 7) / 8 * 8); }
 
@@ -553,13 +569,23 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
     g.K = I;
     g.up_row = 0;
   }
-  if (regime == 0) {
+  if (regime == 0 || regime == 2) {
     g.n_tiles = gemm == 1 ? (g.N + 127) / 128 : (g.N + 255) / 256;
+    // 256-row tiles (large experts, many m-tiles): blocks of four n-tiles,
+    // so a row block is shared by four tiles in flight; 128-row tiles: the
+    // m-tiles of one n-tile run together and share its weights.
+    g.n_group = regime == 2 ? 4 : 1;
     const dim3 grid(round8((long long)max_m_tiles * g.n_tiles));
-    if (gemm == 1) gemm1_swiglu_prefill<<<grid, 256, 0, s>>>(g);
-    else gemm2_down_prefill<<<grid, 256, 0, s>>>(g);
+    if (regime == 0) {
+      if (gemm == 1) gemm1_swiglu_prefill<<<grid, 256, 0, s>>>(g);
+      else gemm2_down_prefill<<<grid, 256, 0, s>>>(g);
+    } else {
+      if (gemm == 1) gemm1_swiglu_wide<<<grid, 256, 0, s>>>(g);
+      else gemm2_down_wide<<<grid, 256, 0, s>>>(g);
+    }
   } else {
     g.n_tiles = (g.N + 127) / 128;
+    g.n_group = 1;
     const dim3 grid(round8((long long)max_m_tiles * g.n_tiles));
     const bool rot = g.K % 2048 == 0;
     if (gemm == 1) {

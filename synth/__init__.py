@@ -6,6 +6,8 @@ from .gen import (
     F32,
     LayerInputs,
     LayerSpec,
+    TraceStep,
+    agentic_trace,
     bf16_bits_to_f32,
     f32_to_bf16_bits,
     logits_of,
@@ -21,6 +23,8 @@ __all__ = [
     "F32",
     "LayerInputs",
     "LayerSpec",
+    "TraceStep",
+    "agentic_trace",
     "bf16_bits_to_f32",
     "f32_to_bf16_bits",
     "logits_of",

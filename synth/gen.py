@@ -61,6 +61,10 @@ CONFIGS = {
     3: LayerSpec(
         "dsv3-share-zipf-bf16", E=256, e0=0, E_loc=32, k=8, H=7168, I=2048, dtype=BF16, T_P=16384, T_D=256, zipf_s=1.2
     ),
+    # the config-2 layer under the agentic trace (agentic_trace): T_P and T_D
+    # here are the token pools the trace's batches are windows of
+    4: LayerSpec("dsv3-share-agentic-bf16", E=256, e0=0, E_loc=32, k=8, H=7168, I=2048, dtype=BF16, T_P=16384,
+                 T_D=256),
 }
 
 
@@ -181,9 +185,56 @@ def make_layer(spec: LayerSpec, seed: int, bias: Optional[np.ndarray] = None) ->
     )
 
 
+# Router biases of the skewed-routing workloads, stored as text (one float32
+# per expert id).  They are calibrated offline against the CPU oracle's
+# routing by tests/golden/make_zipf_bias.py, which documents the target
+# shares; this module only reads them.
+_ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+BIAS_FILES = {3: os.path.join("tests", "golden", "zipf_bias_cfg3.txt")}
+
+
+def stored_bias(cfg: int) -> np.ndarray:
+    b = np.loadtxt(os.path.join(_ROOT, BIAS_FILES[cfg]), dtype=np.float64, comments="#")
+    spec = CONFIGS[cfg]
+    if b.shape != (spec.E,) or not np.all(np.isfinite(b)):
+        raise ValueError(f"bad stored bias for config {cfg}")
+    return b.astype(np.float32)
+
+
 def make_config(cfg: int, seed: Optional[int] = None, bias: Optional[np.ndarray] = None) -> LayerInputs:
     spec = CONFIGS[cfg]
+    if bias is None and cfg in BIAS_FILES:
+        bias = stored_bias(cfg)
     return make_layer(spec, seed_of(cfg) if seed is None else seed, bias=bias)
+
+
+@dataclasses.dataclass(frozen=True)
+class TraceStep:
+    """One step of the agentic rollout trace: a D batch of t_d tokens taken
+    from the D pool at d_off, and (when t_p > 0) a continuation-prefill P
+    batch of t_p tokens taken from the P pool at p_off."""
+
+    t_d: int
+    d_off: int
+    t_p: int
+    p_off: int
+
+
+def agentic_trace(steps: int = 200, seed: int = 1004, pool_p: int = 16384, pool_d: int = 256):
+    """The seeded agentic multi-turn rollout trace: each step runs a D batch
+    of U{32..256} tokens and, with probability 0.5, a P batch whose size is
+    log-uniform on [512, 16384] (rounded).  Batches are windows of fixed
+    token pools at seeded offsets, so replaying the trace draws nothing."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    out = []
+    for _ in range(steps):
+        t_d = int(rng.integers(32, 257))
+        t_p = int(round(math.exp(rng.uniform(math.log(512), math.log(16384))))) if rng.random() < 0.5 else 0
+        t_p = min(t_p, pool_p)
+        d_off = int(rng.integers(0, pool_d - t_d + 1))
+        p_off = int(rng.integers(0, pool_p - t_p + 1)) if t_p else 0
+        out.append(TraceStep(t_d, d_off, t_p, p_off))
+    return out
 
 
 def tie_logits(rng: np.random.Generator, T: int, E: int, levels: int = 4) -> np.ndarray:

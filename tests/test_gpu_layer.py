@@ -53,6 +53,10 @@ SPECS = {
                                                 T_P=50, T_D=3), seed=12),
     "k1-bf16": lambda: make_layer(LayerSpec("k1-bf16", E=16, e0=0, E_loc=16, k=1, H=128, I=128, dtype=BF16, T_P=900,
                                             T_D=2), seed=13),
+    # very large batch (>= 512 rows per expert on average): 256-row tiles for
+    # P, with ragged expert tails, a partial gate/up n-tile and dropped slots
+    "wide-bf16": lambda: make_layer(LayerSpec("wide-bf16", E=8, e0=2, E_loc=4, k=2, H=256, I=192, dtype=BF16,
+                                              T_P=2500, T_D=5), seed=15),
     # k = E: every expert takes every token
     "k-eq-E-bf16": lambda: make_layer(LayerSpec("kE-bf16", E=4, e0=0, E_loc=4, k=4, H=64, I=64, dtype=BF16, T_P=129,
                                                 T_D=1), seed=14),
@@ -244,12 +248,14 @@ def test_state_machine_and_errors():
         g.close()
 
 
-def test_config2_full_size_sampled():
-    """The DeepSeek-V3-shaped share at its full size: routing and layout are
-    checked exactly for every token, x_perm bit-exactly, and the layer output
-    on a sample of tokens (a token's output depends on no other token, so the
-    oracle runs on the sampled sub-batch)."""
-    inp = make_config(2)
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_config_full_size_sampled(cfg):
+    """The DeepSeek-V3-shaped share (config 2) and the same share under
+    Zipf-skewed routing with twice the tokens (config 3) at full size:
+    routing and layout are checked exactly for every token, x_perm
+    bit-exactly, and the layer output on a sample of tokens (a token's output
+    depends on no other token, so the oracle runs on the sampled sub-batch)."""
+    inp = make_config(cfg)
     spec = inp.spec
     g = GpuLayer(inp)
     try:
@@ -262,13 +268,13 @@ def test_config2_full_size_sampled():
             le = oracle.local_map(idx, spec.e0, spec.E_loc)
             counts, offsets, ros, tor = oracle.layout(le, spec.E_loc)
             ref = dict(topk_idx=idx, topk_w=w, counts=counts, offsets=offsets, row_of_slot=ros, token_of_row=tor)
-            assert_route_layout_exact(res, ref, f"cfg2 phase {ph}")
+            assert_route_layout_exact(res, ref, f"cfg{cfg} phase {ph}")
             assert np.array_equal(res["x_perm_raw"], inp.x_bits[ph][tor])
             T = lg.shape[0]
             rng = np.random.default_rng(100 + ph)
             toks = np.sort(rng.choice(T, size=min(T, 40), replace=False))
             sub = oracle.layer(lg[toks], x[toks], inp.w_gu, inp.w_dn, spec.k, spec.e0)
-            assert_close_rms(res["out"][toks], sub["out"], 2e-2, f"cfg2 phase {ph} out (sampled)")
+            assert_close_rms(res["out"][toks], sub["out"], 2e-2, f"cfg{cfg} phase {ph} out (sampled)")
             # h and y of the sampled tokens' rows, reordered into the
             # sub-batch's layout so that its offsets apply
             kept = ros[toks] >= 0
@@ -276,6 +282,6 @@ def test_config2_full_size_sampled():
             rows_sub = sub["row_of_slot"][kept]
             order = np.argsort(rows_sub)
             got = dict(h=res["h"][rows_full[order]], y=res["y"][rows_full[order]])
-            check_h_y(got, sub, inp.w_dn, sub["offsets"], spec, f"cfg2 phase {ph} (sampled rows)")
+            check_h_y(got, sub, inp.w_dn, sub["offsets"], spec, f"cfg{cfg} phase {ph} (sampled rows)")
     finally:
         g.close()

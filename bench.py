@@ -19,7 +19,7 @@ JSON line with:
   steps (the events themselves cost stream time, so the throughput pass runs
   without them) with D-first admission off, so that a P kernel's duration is
   its own work and not the waits the admission policy puts in it;
-* D-first admission (--d-priority-us, default 100): while a D layer is in
+* D-first admission (--d-priority-us, default 300): while a D layer is in
   flight, P grouped-GEMM tiles wait for it, up to that bound; value and
   d_latency_us are measured with it, without_d_first repeats both without;
 * kernels: mean launch duration of every kernel of both phases;
@@ -57,7 +57,7 @@ def parse():
     ap.add_argument("--d-iters", type=int, default=60, help="D layers per latency measurement")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--d-priority-us", type=int, default=100,
+    ap.add_argument("--d-priority-us", type=int, default=300,
                     help="D-first admission: longest wait of a P GEMM tile for an in-flight D layer (0 = off)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="instead of the layer, time a plain device copy of this many MiB (the reference kernel "

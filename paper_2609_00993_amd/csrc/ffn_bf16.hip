@@ -44,7 +44,8 @@ struct GemmArgs {
   const int32_t* tile_base;
   long long b_stride;
   int e_loc, N, K, n_tiles, up_row;
-  int n_group;  // n-tiles per block of the within-expert tile order (see tile_at)
+  int n_group;    // n-tiles per block of the within-expert tile order (see tile_at)
+  int xcd_local;  // 1: consecutive tiles on one XCD (block_tile); 0: dealt round-robin
   YieldTo yield;  // the other phase's layer window to hold back for, if any
 };
 
@@ -90,6 +91,7 @@ __device__ __forceinline__ void tile_at(const GemmArgs& g, int L, int bm, int bn
 // the largest possible tile count, covers every tile.
 __device__ __forceinline__ int block_tile(const GemmArgs& g) {
   const int total = g.tile_base[g.e_loc] * g.n_tiles;
+  if (!g.xcd_local) return (int)blockIdx.x < total ? (int)blockIdx.x : -1;
   const int per_xcd = (total + 7) >> 3;
   const int slot = blockIdx.x >> 3;
   if (slot >= per_xcd) return -1;
@@ -571,10 +573,14 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
   }
   if (regime == 0 || regime == 2) {
     g.n_tiles = gemm == 1 ? (g.N + 127) / 128 : (g.N + 255) / 256;
-    // 256-row tiles (large experts, many m-tiles): blocks of four n-tiles,
-    // so a row block is shared by four tiles in flight; 128-row tiles: the
-    // m-tiles of one n-tile run together and share its weights.
-    g.n_group = regime == 2 ? 4 : 1;
+    // 128-row tiles (a few m-tiles per expert): the m-tiles of one n-tile
+    // run together on one XCD and share its weights in that XCD's L2.
+    // 256-row tiles (large experts, many m-tiles): tiles are dealt to the
+    // XCDs round-robin, so the whole GPU works through one expert at a time
+    // and the expert's weights stay in the memory-side cache; GEMM1 takes
+    // blocks of four n-tiles so a row block is shared by the tiles in flight.
+    g.n_group = regime == 2 ? (gemm == 1 ? 4 : g.n_tiles) : 1;
+    g.xcd_local = regime == 2 ? 0 : 1;
     const dim3 grid(round8((long long)max_m_tiles * g.n_tiles));
     if (regime == 0) {
       if (gemm == 1) gemm1_swiglu_prefill<<<grid, 256, 0, s>>>(g);
@@ -586,6 +592,7 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
   } else {
     g.n_tiles = (g.N + 127) / 128;
     g.n_group = 1;
+    g.xcd_local = 1;
     const dim3 grid(round8((long long)max_m_tiles * g.n_tiles));
     const bool rot = g.K % 2048 == 0;
     if (gemm == 1) {

@@ -35,6 +35,7 @@ namespace moepd {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct GemmArgs {
   const uint16_t* A;       // [R, K] expert-contiguous rows
@@ -435,12 +436,16 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
       }
   };
 
+  // The MFMAs take the weight fragment as their first operand, so each
+  // accumulator holds a transposed 32x32 block: lane l owns output row
+  // (l & 31) and, in registers 4q..4q+3, the four consecutive columns
+  // 8q + 4 (l >> 5) + 0..3 (see the epilogue's vector stores).
   f32x16_t acc[FM][FB];
   auto mfmas = [&](const bf16x8_t (&a)[FM], const bf16x8_t (&b)[FB]) {
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-      for (int j = 0; j < FB; ++j) acc[fm][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[fm], b[j], acc[fm][j], 0, 0, 0);
+      for (int j = 0; j < FB; ++j) acc[fm][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[fm], acc[fm][j], 0, 0, 0);
   };
 
   const int L = block_tile(g);
@@ -505,26 +510,31 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   }
   slice(std::integral_constant<int, 2>{}, kt, slot);
 
-  // epilogue: SwiGLU -> bf16 h, or float32 y.  Rows are checked once per
-  // 32-row block; only the expert's last block checks each row.
+  // epilogue: SwiGLU -> bf16 h (four columns = one 8-byte store), or
+  // float32 y (four columns = one 16-byte store).  A lane's row is fixed,
+  // so it is checked once per 32-row block.  N is a multiple of 64, so a
+  // four-column group is all in range or all out.
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
-    const int rb = tc.m0 + wm * WTM + fm * 32;
-    if (rb >= tc.m_end) continue;
-    const bool full = rb + 32 <= tc.m_end;
+    const int row = tc.m0 + wm * WTM + fm * 32 + (lane & 31);
+    if (row >= tc.m_end) continue;
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
-      const int col = tc.n0 + wn * WTN + fn * 32 + (lane & 31);
-      if (col >= g.N) continue;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int ro = acc_row(r, lane);
-        if (full || rb + ro < tc.m_end) {
-          const size_t at = (size_t)(rb + ro) * g.N + col;
-          if (GATED)
-            static_cast<uint16_t*>(g.C)[at] = f32_to_bf16(silu_mul(acc[fm][fn][r], acc[fm][FN + fn][r]));
-          else
-            static_cast<float*>(g.C)[at] = acc[fm][fn][r];
+      for (int q = 0; q < 4; ++q) {
+        const int col = tc.n0 + wn * WTN + fn * 32 + 8 * q + 4 * (lane >> 5);
+        if (col >= g.N) continue;
+        const size_t at = (size_t)row * g.N + col;
+        if (GATED) {
+          uint32_t lo = f32_to_bf16(silu_mul(acc[fm][fn][4 * q], acc[fm][FN + fn][4 * q]));
+          lo |= (uint32_t)f32_to_bf16(silu_mul(acc[fm][fn][4 * q + 1], acc[fm][FN + fn][4 * q + 1])) << 16;
+          uint32_t hi = f32_to_bf16(silu_mul(acc[fm][fn][4 * q + 2], acc[fm][FN + fn][4 * q + 2]));
+          hi |= (uint32_t)f32_to_bf16(silu_mul(acc[fm][fn][4 * q + 3], acc[fm][FN + fn][4 * q + 3])) << 16;
+          typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+          *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(g.C) + at) = u32x2{lo, hi};
+        } else {
+          f32x4 v = {acc[fm][fn][4 * q], acc[fm][fn][4 * q + 1], acc[fm][fn][4 * q + 2], acc[fm][fn][4 * q + 3]};
+          *reinterpret_cast<f32x4*>(static_cast<float*>(g.C) + at) = v;
         }
       }
     }

@@ -11,7 +11,8 @@ JSON line with:
 
 * value: whole-job layer throughput, (T_P + T_D) * K / wall time of K steps;
 * d_latency_us: the D layer's GPU latency (events on the D stream) alone and
-  while P layers keep the other stream busy, p50/p90/p99;
+  while P layers keep the other stream busy, p50/p90/p99; graph_*: the same
+  with the D layer captured once into a HIP graph and replayed;
 * roofline: the kernel with the largest share of GPU time, its algorithmic
   bytes or flops per launch over its mean launch duration, against the MI355X
   peak that bounds it.  Durations come from HIP events recorded around every
@@ -476,6 +477,42 @@ def main():
 
     lat_alone, _ = d_latencies(False, ctx)
     lat_under, overlapped = d_latencies(True, ctx)
+
+    # ---- the same, with the D layer captured once into a HIP graph and
+    # replayed against its stable phase buffers (the paper's D graph path)
+    def d_graph_latencies(c):
+        sg = torch.cuda.Stream(device=dev)
+        torch.cuda.synchronize()
+        M.layer(c, 1, lg[1], T[1], xs[1], outs[1], sg)  # the phase last ran on the capture stream
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=sg):
+            M.layer(c, 1, lg[1], T[1], xs[1], outs[1], sg)
+        torch.cuda.synchronize()
+        res = {}
+        for under_p in (False, True):
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(args.d_iters)]
+            torch.cuda.synchronize()
+            if under_p:
+                for _ in range(4):
+                    layer(0, c)
+            for a, b in evs:
+                if under_p:
+                    layer(0, c)
+                with torch.cuda.stream(sg):
+                    a.record(sg)
+                    graph.replay()
+                    b.record(sg)
+                if not under_p:
+                    sg.synchronize()
+            torch.cuda.synchronize()
+            res[under_p] = [a.elapsed_time(b) * 1000.0 for a, b in evs]
+        del graph
+        torch.cuda.synchronize()
+        return res
+
+    glat = d_graph_latencies(ctx)
     if ctx_off is not ctx:
         lat_alone_off, _ = d_latencies(False, ctx_off)
         lat_under_off, _ = d_latencies(True, ctx_off)
@@ -539,6 +576,9 @@ def main():
             "p50_under_p": round(p50u, 2), "p90_under_p": round(pct(lat_under, 90), 2),
             "p99_under_p": round(pct(lat_under, 99), 2), "ratio_p50": round(p50u / p50a, 3),
             "iters": args.d_iters, "overlapped_with_p": overlapped,
+            "graph_p50_alone": round(pct(glat[False], 50), 2), "graph_p50_under_p": round(pct(glat[True], 50), 2),
+            "graph_p90_under_p": round(pct(glat[True], 90), 2),
+            "graph_ratio_p50": round(pct(glat[True], 50) / pct(glat[False], 50), 3),
         },
         "roofline": roof,
         "kernels": kernels,

@@ -51,6 +51,16 @@
  *    work and never allocates after moe_ctx_create.  After each call it records
  *    the phase's event on the stream; if the next call on that phase comes on
  *    another stream, that stream first waits on the event.
+ *  - Graph capture (Section 6.1: the D phase replays captured graphs against
+ *    its stable buffers).  A phase's calls may be captured into a HIP graph
+ *    on a stream the phase last ran on: while the stream captures, the
+ *    library records no events and no timing, and a call arriving from
+ *    another stream is refused with MOE_ERR_STATE.  The captured kernels
+ *    carry the batch size and the argument pointers of the capture, and the
+ *    enqueued work issues no memset.  Replays bypass the state machine: the
+ *    caller orders them against the phase's other work and must not reset
+ *    the phase while a replay is in flight.  After a moe_phase_reset, a D
+ *    graph captured earlier no longer opens D-first windows that P honours.
  *  - One host thread may drive a phase at a time; P and D may be driven from
  *    different threads, because their host states are disjoint.
  *  - bf16 data is passed as uint16_t bit patterns (bfloat16), float32 as float.

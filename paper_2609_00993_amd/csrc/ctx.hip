@@ -50,6 +50,8 @@ struct Phase {
   // open.  A reset moves to a new generation, so a window left open by an
   // abandoned layer is no longer honoured.
   int32_t gen = 1;
+  // The current call's stream is being captured into a graph (set by enter).
+  bool capturing = false;
   Timing timing[MOE_NUM_KERNELS];
 };
 
@@ -175,17 +177,30 @@ inline int check_phase(const moe_ctx* ctx, int phase) {
 }
 
 // Order this phase's next work after its previous work when the stream changes.
+// Stream hand-over and graph capture.  A phase driven on a new stream makes
+// that stream wait for the phase's last recorded event.  While `s` is being
+// captured into a graph (a D layer captured once and replayed, Section 6.1),
+// the captured kernels are ordered by the stream itself: no event is
+// recorded or waited on and no timing events are taken, and a hand-over
+// from another stream into a capture is refused (the wait could not be
+// part of the graph): run the phase on the capturing stream first.
 int enter(moe_ctx* ctx, Phase& p, hipStream_t s) {
   if (hipSetDevice(ctx->device) != hipSuccess) return MOE_ERR_HIP;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess) return MOE_ERR_HIP;
+  p.capturing = cs != hipStreamCaptureStatusNone;
   if (p.ev_recorded && p.last_stream != s) {
+    if (p.capturing) return MOE_ERR_STATE;
     if (hipStreamWaitEvent(s, p.ev, 0) != hipSuccess) return MOE_ERR_HIP;
   }
   return MOE_OK;
 }
 
 int leave(Phase& p, hipStream_t s) {
-  if (hipEventRecord(p.ev, s) != hipSuccess) return MOE_ERR_HIP;
-  p.ev_recorded = true;
+  if (!p.capturing) {
+    if (hipEventRecord(p.ev, s) != hipSuccess) return MOE_ERR_HIP;
+    p.ev_recorded = true;
+  }
   p.last_stream = s;
   return MOE_OK;
 }
@@ -194,7 +209,7 @@ int leave(Phase& p, hipStream_t s) {
 template <typename F>
 int timed(Phase& p, int kernel, hipStream_t s, F&& launch) {
   Timing& t = p.timing[kernel];
-  const bool rec = t.capacity > 0 && t.used < t.capacity;
+  const bool rec = !p.capturing && t.capacity > 0 && t.used < t.capacity;
   if (rec && hipEventRecord(t.start[t.used], s) != hipSuccess) return MOE_ERR_HIP;
   if (launch() != hipSuccess) return MOE_ERR_HIP;
   if (rec) {

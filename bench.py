@@ -58,6 +58,9 @@ def parse():
     ap.add_argument("--d-iters", type=int, default=60, help="D layers per latency measurement")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seg-layers", type=int, default=40,
+                    help="MoE layers per P epoch and per D iteration in the segment-policy sweep (0: skip it)")
+    ap.add_argument("--seg-epochs", type=int, default=2, help="P epochs per policy in the segment-policy sweep")
     ap.add_argument("--d-priority-us", type=int, default=300,
                     help="D-first admission: longest wait of a P GEMM tile for an in-flight D layer (0 = off)")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -339,6 +342,124 @@ def run_trace(args, M, inp, dev):
     print(json.dumps(res), flush=True)
 
 
+def segment_sweep(args, M, c, lg, xs, T, spec, sP, dev):
+    """P epochs of `seg_layers` layers run by the native P-epoch runner through
+    the segment turnstile while D iterations (`seg_layers` D layers captured
+    into one HIP graph) run back to back, a D iteration being ready as soon
+    as the previous one has completed.  Policies (Section 7's ordering
+    ladder and Section 7.5's segment sizes): D waits for P's GPU completion
+    (complete), for the whole epoch's host enqueue (enqueue), or for the next
+    permitted boundary with span K = 1..4 (fine-K).  Reports, per policy, D's
+    boundary wait and iteration latency, P's wait for permits and host
+    enqueue time, and the P epoch's makespan (start to GPU completion)."""
+    import torch
+
+    L = args.seg_layers
+    sg = torch.cuda.Stream(device=dev)
+    d_out = torch.empty((T[1], spec.H), dtype=torch.float32, device=dev)
+    p_out = torch.empty((T[0], spec.H), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    M.layer(c, 1, lg[1], T[1], xs[1], d_out, sg)  # the D phase last ran on the capture stream
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=sg):
+        for _ in range(L):
+            M.layer(c, 1, lg[1], T[1], xs[1], d_out, sg)
+    torch.cuda.synchronize()
+
+    def d_iteration():
+        with torch.cuda.stream(sg):
+            graph.replay()
+            ev = torch.cuda.Event()
+            ev.record(sg)
+        return ev
+
+    alone = []
+    for _ in range(5):
+        t0 = time.perf_counter()
+        d_iteration().synchronize()
+        alone.append((time.perf_counter() - t0) * 1e6)
+    p_alone = []
+    for _ in range(2):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(L):
+            M.layer(c, 0, lg[0], T[0], xs[0], p_out, sP)
+        sP.synchronize()
+        p_alone.append((time.perf_counter() - t0) * 1e6)
+
+    policies = [("complete", L + 1), ("enqueue", L + 1)] + [(f"fine-{k}", k) for k in (1, 2, 3, 4)]
+    out = {}
+    epoch = 0
+    for name, K in policies:
+        st, ts = M.moe_turnstile_create(K, 0)
+        M.check(st, "moe_turnstile_create")
+        waits, lats, make, p_wait, p_enq, rounds = [], [], [], [], [], []
+        t_policy = time.perf_counter()
+        prev = d_iteration()
+        t_ready = None
+        try:
+            for _ in range(args.seg_epochs):
+                t_start = time.perf_counter()
+                st, runner = M.moe_p_epoch_start(c, ts, epoch, True, T[0], [lg[0]] * L, [xs[0]] * L, [p_out] * L, sP,
+                                                 60_000_000)
+                M.check(st, "moe_p_epoch_start")
+                epoch += 1
+                joined = None
+                while True:
+                    prev.synchronize()
+                    now = time.perf_counter()
+                    if t_ready is not None:
+                        lats.append((now - t_ready) * 1e6)
+                    t_ready = now
+                    M.check(M.moe_turnstile_wait_boundary(ts, 60_000_000), "wait_boundary")
+                    done = M.moe_turnstile_query(ts)[1].task == M.MOE_TS_DONE
+                    if done:
+                        joined = M.moe_p_epoch_join(runner)
+                        if name == "complete":
+                            sP.synchronize()
+                    waits.append((time.perf_counter() - t_ready) * 1e6)
+                    prev = d_iteration()
+                    M.check(M.moe_turnstile_release(ts))
+                    if done:
+                        break
+                st, stats = joined
+                M.check(st, "P epoch")
+                q = M.moe_turnstile_query(ts)[1]
+                rounds.append(q.rounds)
+                sP.synchronize()
+                make.append((time.perf_counter() - t_start) * 1e6)
+                p_wait.append(stats.wait_us)
+                p_enq.append(stats.enqueue_us)
+            prev.synchronize()
+            lats.append((time.perf_counter() - t_ready) * 1e6)
+            t_ready = None
+            wall = time.perf_counter() - t_policy
+        finally:
+            M.moe_turnstile_destroy(ts)
+        out[name] = {
+            "span": K if name.startswith("fine") else None,
+            "d_wait_us_mean": round(sum(waits) / len(waits), 1), "d_wait_us_p99": round(pct(waits, 99), 1),
+            "d_iter_us_p50": round(pct(lats, 50), 1), "d_iter_us_p99": round(pct(lats, 99), 1),
+            "d_iters_per_epoch": round(len(waits) / args.seg_epochs, 1),
+            "p_epoch_ms": round(sum(make) / len(make) / 1e3, 3),
+            "p_wait_for_permit_ms": round(sum(p_wait) / len(p_wait) / 1e3, 3),
+            "p_enqueue_ms": round(sum(p_enq) / len(p_enq) / 1e3, 3),
+            "rounds_per_epoch": sum(rounds) / len(rounds),
+            "wall_ms": round(wall * 1e3, 2),
+            "p_layer_tokens_per_s": round(T[0] * L * args.seg_epochs / wall, 1),
+            "d_layer_tokens_per_s": round(T[1] * L * (len(waits) + 1) / wall, 1),
+        }
+        print(f"# segments {name}: {out[name]}", file=sys.stderr, flush=True)
+    del graph
+    torch.cuda.synchronize()
+    return {"layers": L, "epochs_per_policy": args.seg_epochs, "d_iter_alone_us_p50": round(pct(alone, 50), 1),
+            "p_epoch_alone_ms": round(min(p_alone) / 1e3, 3), "policies": out,
+            "note": "one P epoch = L layers of the P batch (one boundary per layer, after its dispatch layout); one D "
+                    "iteration = L layers of the D batch replayed as one HIP graph, ready when the previous one "
+                    "completes; D-first admission as in the bench line"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -513,6 +634,7 @@ def main():
         return res
 
     glat = d_graph_latencies(ctx)
+    segments = segment_sweep(args, M, ctx, lg, xs, T, spec, sP, dev) if args.seg_layers > 0 else None
     if ctx_off is not ctx:
         lat_alone_off, _ = d_latencies(False, ctx_off)
         lat_under_off, _ = d_latencies(True, ctx_off)
@@ -581,6 +703,7 @@ def main():
             "graph_ratio_p50": round(pct(glat[True], 50) / pct(glat[False], 50), 3),
         },
         "roofline": roof,
+        "segments": segments,
         "kernels": kernels,
         "kernels_pass_ms_per_step": round(wall_events / args.steps * 1e3, 4),
         "kernels_pass_note": "per-kernel HIP events over a second pass of the same concurrent steps, D-first admission "

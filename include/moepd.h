@@ -18,7 +18,10 @@
  *  - Section 5.2: normal dispatch is split after expert notification, when
  *    the dispatch shape (per-expert counts) is known and before routed data
  *    moves.  moe_dispatch runs the notification part (histogram and prefix
- *    sum, the layout) and then the data movement (token permutation).
+ *    sum, the layout) and then the data movement (token permutation);
+ *    moe_dispatch_layout and moe_dispatch_permute are the two halves, so a
+ *    caller can stop at the boundary between them (a safe P boundary,
+ *    Section 4.2) and let other work in before any routed data moves.
  *  - Section 5.2: at most one pending operation per phase buffer, with
  *    explicit transitions so that cancellation never reuses partially
  *    advanced state (the per-phase state machine and moe_phase_reset).
@@ -96,8 +99,16 @@ enum {
 };
 
 /* Per-phase state machine: IDLE -route-> ROUTED -dispatch-> DISPATCHED
- * -expert_ffn-> COMPUTED -combine-> IDLE. */
-enum { MOE_STATE_IDLE = 0, MOE_STATE_ROUTED = 1, MOE_STATE_DISPATCHED = 2, MOE_STATE_COMPUTED = 3 };
+ * -expert_ffn-> COMPUTED -combine-> IDLE, where the dispatch step may be
+ * taken in two: ROUTED -dispatch_layout-> LAID_OUT -dispatch_permute->
+ * DISPATCHED. */
+enum {
+  MOE_STATE_IDLE = 0,
+  MOE_STATE_ROUTED = 1,
+  MOE_STATE_DISPATCHED = 2,
+  MOE_STATE_COMPUTED = 3,
+  MOE_STATE_LAID_OUT = 4
+};
 
 /* Kernels whose launches can be timed (moe_timing_*). */
 enum {
@@ -191,6 +202,22 @@ int moe_route(moe_ctx_t* ctx, int phase, const float* logits, int32_t T, hipStre
  * preceding moe_route).  Errors: MOE_ERR_INVALID_ARG (null x with T > 0),
  * MOE_ERR_INVALID_PHASE, MOE_ERR_STATE, MOE_ERR_HIP. */
 int moe_dispatch(moe_ctx_t* ctx, int phase, const void* x, hipStream_t stream);
+
+/* The notification half of moe_dispatch (ROUTED -> LAID_OUT, Section 5.2):
+ * enqueues the histogram and the layout (counts, offsets, row_of_slot,
+ * token_of_row) and moves no token data.  Once it returns the dispatch shape
+ * is fixed on the stream; the phase may wait here, at a safe boundary, for as
+ * long as the caller likes.  Errors: MOE_ERR_INVALID_ARG (null stream),
+ * MOE_ERR_INVALID_PHASE, MOE_ERR_STATE, MOE_ERR_HIP. */
+int moe_dispatch_layout(moe_ctx_t* ctx, int phase, hipStream_t stream);
+
+/* The data half of moe_dispatch (LAID_OUT -> DISPATCHED): copies x[t] into
+ * x_perm[row] for every resident slot, using the layout enqueued by
+ * moe_dispatch_layout.  x as for moe_dispatch.  moe_dispatch_layout followed
+ * by moe_dispatch_permute enqueues exactly the kernels of moe_dispatch.
+ * Errors: MOE_ERR_INVALID_ARG (null x with T > 0, null stream),
+ * MOE_ERR_INVALID_PHASE, MOE_ERR_STATE, MOE_ERR_HIP. */
+int moe_dispatch_permute(moe_ctx_t* ctx, int phase, const void* x, hipStream_t stream);
 
 /* Grouped expert FFN (DISPATCHED -> COMPUTED): h = silu(x_perm W1^T) *
  * (x_perm W3^T) and y = h W2^T for the rows of every resident expert.  bf16

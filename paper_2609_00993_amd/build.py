@@ -40,8 +40,30 @@ CFLAGS = [
 ]
 
 
+# Host-only sources (the turnstile and the P-epoch runner) take the host
+# compiler: they include the HIP runtime API but hold no device code.
+CXX = os.environ.get("CXX", "g++")
+HOST_CFLAGS = [
+    "-O2",
+    "-std=c++17",
+    "-fPIC",
+    "-Wall",
+    "-pthread",
+    "-D__HIP_PLATFORM_AMD__",
+    f"-I{os.environ.get('ROCM_PATH', '/opt/rocm')}/include",
+    f"-I{INCLUDE}",
+    f"-I{CSRC}",
+]
+
+
 def sources():
-    return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
+    return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hip", ".cpp")))
+
+
+def _compile_cmd(src, obj):
+    if src.endswith(".cpp"):
+        return [CXX, *HOST_CFLAGS, "-c", src, "-o", obj]
+    return [HIPCC, *CFLAGS, "-c", src, "-o", obj]
 
 
 def _run(cmd):
@@ -55,8 +77,8 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
         raise RuntimeError(f"hipcc not found at {HIPCC}")
     os.makedirs(BUILD, exist_ok=True)
     srcs = sources()
-    objs = [os.path.join(BUILD, os.path.basename(s).replace(".hip", ".o")) for s in srcs]
-    cmds = [[HIPCC, *CFLAGS, "-c", s, "-o", o] for s, o in zip(srcs, objs)]
+    objs = [os.path.join(BUILD, os.path.splitext(os.path.basename(s))[0] + ".o") for s in srcs]
+    cmds = [_compile_cmd(s, o) for s, o in zip(srcs, objs)]
     with cf.ThreadPoolExecutor(max_workers=min(jobs, len(cmds))) as ex:
         results = list(ex.map(_run, cmds))
     for cmd, (rc, out) in zip(cmds, results):
@@ -67,7 +89,7 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
         if rc:
             raise RuntimeError(f"compile failed: {cmd[-3]}")
     tmp = LIB + ".tmp"
-    rc, out = _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
+    rc, out = _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-pthread", "-o", tmp, *objs])
     if rc:
         print(out)
         raise RuntimeError("link failed")

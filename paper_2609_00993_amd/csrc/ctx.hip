@@ -16,6 +16,7 @@
 
 #include "kernels.h"
 #include "moepd.h"
+#include "moepd_turnstile.h"
 
 using namespace moepd;
 
@@ -236,6 +237,40 @@ YieldTo yield_of(moe_ctx* ctx, int phase) {
   const Phase& d = ctx->ph[MOE_PHASE_D];
   return YieldTo{d.b.signal, d.gen, (ctx->cfg.d_priority_us * 10 + 33) / 34};
 }
+// Dispatch notification (Section 5.2): the per-chunk histogram, then the
+// prefix sum and stable row assignment.  Picks the phase's tile regime.
+int layout(moe_ctx* ctx, Phase& p, hipStream_t stream) {
+  const moe_config_t& c = ctx->cfg;
+  const int T = p.T, k = c.top_k, E_loc = c.num_local_experts;
+  chunking(T, k, E_loc, &p.chunk_tokens, &p.nchunks);
+  if (c.dtype == MOE_DTYPE_BF16) {
+    // Rows per resident expert expected under even routing: T*k/E.  Small
+    // batches stream weights (32-row tiles); large ones take 128-row tiles,
+    // and very large ones 256-row tiles, which move a third fewer bytes into
+    // LDS per flop.
+    const long long avg = (long long)T * k / c.num_experts;
+    p.regime = avg >= 512 ? 2 : avg >= 32 ? 0 : 1;
+    p.bm = ffn_bf16_bm(p.regime);
+  } else {
+    p.regime = 0;
+    p.bm = ffn_f32_bm();
+  }
+  int st = timed(p, MOE_KERNEL_COUNT, stream, [&] {
+    return launch_count(p.b.topk_idx, T, k, c.expert_begin, E_loc, p.chunk_tokens, p.nchunks, p.b, stream);
+  });
+  if (st) return st;
+  return timed(p, MOE_KERNEL_PLACE, stream, [&] {
+    return launch_place(p.b.topk_idx, T, k, c.expert_begin, E_loc, p.chunk_tokens, p.nchunks, p.bm, p.b, stream);
+  });
+}
+
+// Dispatch data movement: token rows into expert-contiguous rows.
+int permute(moe_ctx* ctx, Phase& p, const void* x, hipStream_t stream) {
+  if (p.T == 0) return MOE_OK;
+  return timed(p, MOE_KERNEL_PERMUTE, stream, [&] {
+    return launch_permute(x, p.T, ctx->cfg.top_k, ctx->cfg.hidden * ctx->esz, p.b.row_of_slot, p.b.x_perm, stream);
+  });
+}
 }  // namespace
 
 extern "C" {
@@ -289,6 +324,33 @@ int moe_route(moe_ctx_t* ctx, int phase, const float* logits, int32_t T, hipStre
   return MOE_OK;
 }
 
+int moe_dispatch_layout(moe_ctx_t* ctx, int phase, hipStream_t stream) {
+  int st = check_phase(ctx, phase);
+  if (st) return st;
+  Phase& p = ctx->ph[phase];
+  if (!stream) return MOE_ERR_INVALID_ARG;
+  if (p.state != MOE_STATE_ROUTED) return MOE_ERR_STATE;
+  if ((st = enter(ctx, p, stream))) return st;
+  if ((st = layout(ctx, p, stream))) return st;
+  if ((st = leave(p, stream))) return st;
+  p.state = MOE_STATE_LAID_OUT;
+  return MOE_OK;
+}
+
+int moe_dispatch_permute(moe_ctx_t* ctx, int phase, const void* x, hipStream_t stream) {
+  int st = check_phase(ctx, phase);
+  if (st) return st;
+  Phase& p = ctx->ph[phase];
+  if (!stream) return MOE_ERR_INVALID_ARG;
+  if (p.state != MOE_STATE_LAID_OUT) return MOE_ERR_STATE;
+  if (p.T > 0 && !x) return MOE_ERR_INVALID_ARG;
+  if ((st = enter(ctx, p, stream))) return st;
+  if ((st = permute(ctx, p, x, stream))) return st;
+  if ((st = leave(p, stream))) return st;
+  p.state = MOE_STATE_DISPATCHED;
+  return MOE_OK;
+}
+
 int moe_dispatch(moe_ctx_t* ctx, int phase, const void* x, hipStream_t stream) {
   int st = check_phase(ctx, phase);
   if (st) return st;
@@ -297,35 +359,8 @@ int moe_dispatch(moe_ctx_t* ctx, int phase, const void* x, hipStream_t stream) {
   if (p.state != MOE_STATE_ROUTED) return MOE_ERR_STATE;
   if (p.T > 0 && !x) return MOE_ERR_INVALID_ARG;
   if ((st = enter(ctx, p, stream))) return st;
-  const moe_config_t& c = ctx->cfg;
-  const int T = p.T, k = c.top_k, E_loc = c.num_local_experts;
-  chunking(T, k, E_loc, &p.chunk_tokens, &p.nchunks);
-  if (c.dtype == MOE_DTYPE_BF16) {
-    // Rows per resident expert expected under even routing: T*k/E.  Small
-    // batches stream weights (32-row tiles); large ones take 128-row tiles,
-    // and very large ones 256-row tiles, which move a third fewer bytes into
-    // LDS per flop.
-    const long long avg = (long long)T * k / c.num_experts;
-    p.regime = avg >= 512 ? 2 : avg >= 32 ? 0 : 1;
-    p.bm = ffn_bf16_bm(p.regime);
-  } else {
-    p.regime = 0;
-    p.bm = ffn_f32_bm();
-  }
-  st = timed(p, MOE_KERNEL_COUNT, stream, [&] {
-    return launch_count(p.b.topk_idx, T, k, c.expert_begin, E_loc, p.chunk_tokens, p.nchunks, p.b, stream);
-  });
-  if (st) return st;
-  st = timed(p, MOE_KERNEL_PLACE, stream, [&] {
-    return launch_place(p.b.topk_idx, T, k, c.expert_begin, E_loc, p.chunk_tokens, p.nchunks, p.bm, p.b, stream);
-  });
-  if (st) return st;
-  if (T > 0) {
-    st = timed(p, MOE_KERNEL_PERMUTE, stream, [&] {
-      return launch_permute(x, T, k, c.hidden * ctx->esz, p.b.row_of_slot, p.b.x_perm, stream);
-    });
-    if (st) return st;
-  }
+  if ((st = layout(ctx, p, stream))) return st;
+  if ((st = permute(ctx, p, x, stream))) return st;
   if ((st = leave(p, stream))) return st;
   p.state = MOE_STATE_DISPATCHED;
   return MOE_OK;
@@ -439,6 +474,8 @@ const char* moe_status_string(int status) {
     case MOE_ERR_BUSY: return "phase has work in flight";
     case MOE_ERR_OOM: return "device allocation failed";
     case MOE_ERR_HIP: return "HIP runtime error";
+    case MOE_ERR_REJECTED: return "turnstile refused the call";
+    case MOE_ERR_TIMEOUT: return "turnstile wait timed out";
     default: return "unknown status";
   }
 }

@@ -1,4 +1,5 @@
-"""Thin ctypes binding of libmoepd (the C ABI declared in include/moepd.h).
+"""Thin ctypes binding of libmoepd (the C ABI declared in include/moepd.h and
+include/moepd_turnstile.h).
 
 Argument marshalling only: every step of the layer runs in the HIP library.
 Device buffers may be passed as integers (device addresses) or as objects
@@ -16,7 +17,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, byref, c_char_p, c_double, c_int, c_int32, c_void_p
+from ctypes import POINTER, byref, c_char_p, c_double, c_int, c_int32, c_int64, c_void_p
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libmoepd.so")
@@ -32,8 +33,13 @@ MOE_ERR_STATE = -4
 MOE_ERR_BUSY = -5
 MOE_ERR_OOM = -6
 MOE_ERR_HIP = -7
+MOE_ERR_REJECTED = -8
+MOE_ERR_TIMEOUT = -9
 
-MOE_STATE_IDLE, MOE_STATE_ROUTED, MOE_STATE_DISPATCHED, MOE_STATE_COMPUTED = 0, 1, 2, 3
+MOE_TS_IDLE, MOE_TS_ACTIVE, MOE_TS_DONE = 0, 1, 2
+MOE_TS_EV_BEGIN, MOE_TS_EV_PUBLISH, MOE_TS_EV_RESUME, MOE_TS_EV_ENTER, MOE_TS_EV_RELEASE, MOE_TS_EV_DONE = range(6)
+
+MOE_STATE_IDLE, MOE_STATE_ROUTED, MOE_STATE_DISPATCHED, MOE_STATE_COMPUTED, MOE_STATE_LAID_OUT = 0, 1, 2, 3, 4
 
 MOE_KERNEL_ROUTE = 0
 MOE_KERNEL_COUNT = 1
@@ -82,11 +88,45 @@ class moe_phase_view_t(ctypes.Structure):
     ]
 
 
-# Every symbol the header declares, with its ctypes signature.
+class moe_turnstile_state_t(ctypes.Structure):
+    _fields_ = [
+        ("epoch", c_int64),
+        ("reached", c_int64),
+        ("permit", c_int64),
+        ("span", c_int32),
+        ("task", c_int32),
+        ("rounds", c_int64),
+        ("rejected", c_int64),
+        ("p_wait_us", c_double),
+        ("d_wait_us", c_double),
+        ("d_entries", c_int64),
+        ("log_dropped", c_int64),
+    ]
+
+
+class moe_turnstile_event_t(ctypes.Structure):
+    _fields_ = [("kind", c_int32), ("reserved", c_int32), ("epoch", c_int64), ("value", c_int64),
+                ("t_ns", c_int64)]
+
+
+class moe_p_epoch_stats_t(ctypes.Structure):
+    _fields_ = [
+        ("status", c_int32),
+        ("layers_done", c_int32),
+        ("enqueue_us", c_double),
+        ("wait_us", c_double),
+        ("t_begin_ns", c_int64),
+        ("t_end_ns", c_int64),
+    ]
+
+
+# Every symbol the headers declare, with its ctypes signature.
 _SIGNATURES = {
     "moe_ctx_create": (c_int, [POINTER(moe_config_t), POINTER(moe_weights_t), POINTER(c_void_p)]),
     "moe_route": (c_int, [c_void_p, c_int, c_void_p, c_int32, c_void_p]),
     "moe_dispatch": (c_int, [c_void_p, c_int, c_void_p, c_void_p]),
+    "moe_dispatch_layout": (c_int, [c_void_p, c_int, c_void_p]),
+    "moe_dispatch_permute": (c_int, [c_void_p, c_int, c_void_p, c_void_p]),
     "moe_expert_ffn": (c_int, [c_void_p, c_int, c_void_p]),
     "moe_combine": (c_int, [c_void_p, c_int, c_void_p, c_void_p]),
     "moe_phase_view": (c_int, [c_void_p, c_int, POINTER(moe_phase_view_t)]),
@@ -96,11 +136,34 @@ _SIGNATURES = {
     "moe_timing_enable": (c_int, [c_void_p, c_int32]),
     "moe_timing_read": (c_int, [c_void_p, c_int, c_int, POINTER(c_double), POINTER(c_int32)]),
     "moe_kernel_name": (c_char_p, [c_int]),
+    "moe_turnstile_create": (c_int, [c_int32, c_int32, POINTER(c_void_p)]),
+    "moe_turnstile_destroy": (c_int, [c_void_p]),
+    "moe_turnstile_set_span": (c_int, [c_void_p, c_int32]),
+    "moe_turnstile_begin": (c_int, [c_void_p, c_int64, c_int32]),
+    "moe_turnstile_publish": (c_int, [c_void_p, c_int64, c_int64]),
+    "moe_turnstile_wait_permit": (c_int, [c_void_p, c_int64, c_int64, c_int64]),
+    "moe_turnstile_done": (c_int, [c_void_p, c_int64]),
+    "moe_turnstile_wait_boundary": (c_int, [c_void_p, c_int64]),
+    "moe_turnstile_release": (c_int, [c_void_p]),
+    "moe_turnstile_query": (c_int, [c_void_p, POINTER(moe_turnstile_state_t)]),
+    "moe_turnstile_log": (c_int, [c_void_p, POINTER(moe_turnstile_event_t), c_int32, POINTER(c_int32)]),
+    "moe_p_epoch_start": (c_int, [c_void_p, c_void_p, c_int64, c_int32, c_int32, c_int32, POINTER(c_void_p),
+                                  POINTER(c_void_p), POINTER(c_void_p), c_void_p, c_int64, POINTER(c_void_p)]),
+    "moe_p_epoch_join": (c_int, [c_void_p, POINTER(moe_p_epoch_stats_t)]),
 }
 SYMBOLS = tuple(_SIGNATURES)
 
 
 def _load():
+    # The library links the HIP runtime by its soname.  PyTorch's ROCm wheel
+    # carries its own copy of that runtime; when torch is loaded first, the
+    # dynamic linker binds the library to the copy already in the process,
+    # so torch's allocations and streams and the library's calls share one
+    # runtime.  Loaded the other way round, the process would hold two.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     if not os.path.exists(LIB_PATH):
         raise ImportError(
             f"libmoepd.so is not built ({LIB_PATH} missing); run `python -m paper_2609_00993_amd.build`")
@@ -174,6 +237,14 @@ def moe_dispatch(ctx, phase: int, x, stream) -> int:
     return _lib.moe_dispatch(ctx, phase, _ptr(x), _stream(stream))
 
 
+def moe_dispatch_layout(ctx, phase: int, stream) -> int:
+    return _lib.moe_dispatch_layout(ctx, phase, _stream(stream))
+
+
+def moe_dispatch_permute(ctx, phase: int, x, stream) -> int:
+    return _lib.moe_dispatch_permute(ctx, phase, _ptr(x), _stream(stream))
+
+
 def moe_expert_ffn(ctx, phase: int, stream) -> int:
     return _lib.moe_expert_ffn(ctx, phase, _stream(stream))
 
@@ -213,6 +284,79 @@ def moe_timing_read(ctx, phase: int, kernel: int):
 
 def moe_kernel_name(kernel: int) -> str:
     return _lib.moe_kernel_name(kernel).decode()
+
+
+# ---- turnstile (include/moepd_turnstile.h) ----
+
+def moe_turnstile_create(span: int, log_capacity: int = 0):
+    out = c_void_p()
+    st = _lib.moe_turnstile_create(span, log_capacity, byref(out))
+    return st, out.value
+
+
+def moe_turnstile_destroy(ts) -> int:
+    return _lib.moe_turnstile_destroy(ts)
+
+
+def moe_turnstile_set_span(ts, span: int) -> int:
+    return _lib.moe_turnstile_set_span(ts, span)
+
+
+def moe_turnstile_begin(ts, epoch: int, d_enqueued: bool) -> int:
+    return _lib.moe_turnstile_begin(ts, epoch, int(bool(d_enqueued)))
+
+
+def moe_turnstile_publish(ts, epoch: int, boundary: int) -> int:
+    return _lib.moe_turnstile_publish(ts, epoch, boundary)
+
+
+def moe_turnstile_wait_permit(ts, epoch: int, boundary: int, timeout_us: int) -> int:
+    return _lib.moe_turnstile_wait_permit(ts, epoch, boundary, timeout_us)
+
+
+def moe_turnstile_done(ts, epoch: int) -> int:
+    return _lib.moe_turnstile_done(ts, epoch)
+
+
+def moe_turnstile_wait_boundary(ts, timeout_us: int) -> int:
+    return _lib.moe_turnstile_wait_boundary(ts, timeout_us)
+
+
+def moe_turnstile_release(ts) -> int:
+    return _lib.moe_turnstile_release(ts)
+
+
+def moe_turnstile_query(ts):
+    q = moe_turnstile_state_t()
+    st = _lib.moe_turnstile_query(ts, byref(q))
+    return st, q
+
+
+def moe_turnstile_log(ts, capacity: int = 4096):
+    """(status, [(kind, epoch, value, t_ns), ...]) of the events moved out of the log."""
+    buf = (moe_turnstile_event_t * max(capacity, 1))()
+    n = c_int32()
+    st = _lib.moe_turnstile_log(ts, buf, capacity, byref(n))
+    return st, [(buf[i].kind, buf[i].epoch, buf[i].value, buf[i].t_ns) for i in range(n.value)]
+
+
+def moe_p_epoch_start(ctx, ts, epoch: int, d_enqueued: bool, T: int, logits, x, out, stream, timeout_us: int):
+    """Start a P-epoch runner over len(logits) layers; logits, x and out are
+    sequences of device buffers (one per layer).  Returns (status, runner)."""
+    L = len(logits)
+    if len(x) != L or len(out) != L:
+        return MOE_ERR_INVALID_ARG, None
+    arr = lambda seq: (c_void_p * L)(*[_ptr(b) for b in seq])
+    r = c_void_p()
+    st = _lib.moe_p_epoch_start(ctx, ts, epoch, int(bool(d_enqueued)), L, T, arr(logits), arr(x), arr(out),
+                                _stream(stream), timeout_us, byref(r))
+    return st, r.value
+
+
+def moe_p_epoch_join(runner):
+    s = moe_p_epoch_stats_t()
+    st = _lib.moe_p_epoch_join(runner, byref(s))
+    return st, s
 
 
 def layer(ctx, phase: int, logits, T: int, x, out, stream) -> None:

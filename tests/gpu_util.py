@@ -22,6 +22,15 @@ def hip():
     return _hip
 
 
+def hip_last_error() -> str:
+    h = hip()
+    h.hipGetLastError.restype = ctypes.c_int
+    h.hipGetErrorString.restype = ctypes.c_char_p
+    h.hipGetErrorString.argtypes = [ctypes.c_int]
+    e = h.hipGetLastError()
+    return f"{e} ({h.hipGetErrorString(e).decode()})"
+
+
 def read_dev(ptr: int, shape, dtype) -> np.ndarray:
     """Copy device memory at `ptr` into a new host array (after a device sync)."""
     a = np.empty(shape, dtype)
@@ -68,6 +77,9 @@ class GpuLayer:
                             M.MOE_DTYPE_BF16 if self.bf16 else M.MOE_DTYPE_F32, max_tokens[0], max_tokens[1],
                             d_priority_us=d_priority_us)
         st, self.ctx = M.moe_ctx_create(cfg, self.w_gu, self.w_dn)
+        if st == M.MOE_ERR_HIP:
+            err = hip_last_error()
+            raise AssertionError(f"moe_ctx_create: HIP error {err} (free/total {torch.cuda.mem_get_info()})")
         M.check(st, "moe_ctx_create")
         self.streams = {0: torch.cuda.Stream(), 1: torch.cuda.Stream()}
 

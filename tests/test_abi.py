@@ -1,6 +1,7 @@
-"""The C-ABI library loads and exports every function include/moepd.h declares,
+"""The C-ABI library loads and exports every function include/*.h declares,
 and its host-side validation answers without touching a GPU."""
 
+import glob
 import os
 import re
 import subprocess
@@ -8,12 +9,12 @@ import subprocess
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "moepd.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 LIB = os.path.join(ROOT, "paper_2609_00993_amd", "libmoepd.so")
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "\n".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(moe_\w+)\s*\(", text, flags=re.M)))
 
@@ -21,7 +22,8 @@ def declared_functions():
 def test_header_declares_the_layer_calls():
     names = declared_functions()
     for n in ("moe_ctx_create", "moe_route", "moe_dispatch", "moe_expert_ffn", "moe_combine", "moe_phase_view",
-              "moe_phase_reset", "moe_ctx_destroy", "moe_status_string"):
+              "moe_phase_reset", "moe_ctx_destroy", "moe_status_string", "moe_dispatch_layout",
+              "moe_dispatch_permute", "moe_turnstile_create", "moe_p_epoch_start", "moe_p_epoch_join"):
         assert n in names
 
 
@@ -43,7 +45,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_status_strings(lib):
-    for code in range(-7, 1):
+    for code in range(-9, 1):
         s = lib.moe_status_string(code)
         assert s and s != "unknown status"
     assert lib.moe_status_string(-99) == "unknown status"
@@ -87,3 +89,25 @@ def test_null_context_calls(lib):
     assert lib.moe_timing_enable(None, 4) == lib.MOE_ERR_INVALID_ARG
     assert lib.moe_timing_read(None, 0, 0)[0] == lib.MOE_ERR_INVALID_ARG
     assert lib.moe_ctx_destroy(None) == lib.MOE_OK
+    assert lib.moe_dispatch_layout(None, 0, 1) == lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_dispatch_permute(None, 0, 0, 1) == lib.MOE_ERR_INVALID_ARG
+
+
+def test_p_epoch_runner_validates_before_touching_the_gpu(lib):
+    st, ts = lib.moe_turnstile_create(1, 0)
+    lib.check(st)
+    try:
+        bufs = [0x1000] * 2
+        assert lib.moe_p_epoch_start(None, ts, 0, True, 4, bufs, bufs, bufs, 1, 1000)[0] == lib.MOE_ERR_INVALID_ARG
+        assert lib.moe_p_epoch_start(0x10, None, 0, True, 4, bufs, bufs, bufs, 1, 1000)[0] == lib.MOE_ERR_INVALID_ARG
+        assert lib.moe_p_epoch_start(0x10, ts, 0, True, 4, bufs, bufs, bufs, 0, 1000)[0] == lib.MOE_ERR_INVALID_ARG
+        assert lib.moe_p_epoch_start(0x10, ts, 0, True, 4, bufs, bufs, bufs, 1, 0)[0] == lib.MOE_ERR_INVALID_ARG
+        assert lib.moe_p_epoch_start(0x10, ts, 0, True, -1, bufs, bufs, bufs, 1, 1000)[0] == lib.MOE_ERR_INVALID_ARG
+        assert lib.moe_p_epoch_start(0x10, ts, 0, True, 4, bufs, [0x1000, 0], bufs, 1, 1000)[0] == \
+            lib.MOE_ERR_INVALID_ARG
+        assert lib.moe_p_epoch_start(0x10, ts, 0, True, 4, [], [], [], 1, 1000)[0] == lib.MOE_ERR_INVALID_ARG
+        assert lib.moe_p_epoch_join(None)[0] == lib.MOE_ERR_INVALID_ARG
+        st, q = lib.moe_turnstile_query(ts)
+        assert q.task == lib.MOE_TS_IDLE and q.epoch == -1  # nothing began
+    finally:
+        lib.moe_turnstile_destroy(ts)

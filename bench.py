@@ -347,7 +347,7 @@ def segment_sweep(args, M, c, lg, xs, T, spec, sP, dev):
     the segment turnstile while D iterations (`seg_layers` D layers captured
     into one HIP graph) run back to back, a D iteration being ready as soon
     as the previous one has completed.  Policies (Section 7's ordering
-    ladder and Section 7.5's segment sizes): D waits for P's GPU completion
+    ladder and Section 7.6's segment sizes): D waits for P's GPU completion
     (complete), for the whole epoch's host enqueue (enqueue), or for the next
     permitted boundary with span K = 1..4 (fine-K).  Reports, per policy, D's
     boundary wait and iteration latency, P's wait for permits and host
@@ -369,16 +369,17 @@ def segment_sweep(args, M, c, lg, xs, T, spec, sP, dev):
 
     def d_iteration():
         with torch.cuda.stream(sg):
+            start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            start.record(sg)
             graph.replay()
-            ev = torch.cuda.Event()
-            ev.record(sg)
-        return ev
+            end.record(sg)
+        return start, end
 
     alone = []
     for _ in range(5):
-        t0 = time.perf_counter()
-        d_iteration().synchronize()
-        alone.append((time.perf_counter() - t0) * 1e6)
+        start, end = d_iteration()
+        end.synchronize()
+        alone.append(start.elapsed_time(end) * 1e3)
     p_alone = []
     for _ in range(2):
         torch.cuda.synchronize()
@@ -388,30 +389,32 @@ def segment_sweep(args, M, c, lg, xs, T, spec, sP, dev):
         sP.synchronize()
         p_alone.append((time.perf_counter() - t0) * 1e6)
 
+    # D latency of an iteration = its boundary wait (host, from the moment the
+    # previous iteration completed) + its GPU span (events around the replay).
+    # P's epoch span is taken on the P stream, from an event enqueued before
+    # the runner starts to one enqueued after it has finished.
     policies = [("complete", L + 1), ("enqueue", L + 1)] + [(f"fine-{k}", k) for k in (1, 2, 3, 4)]
     out = {}
     epoch = 0
     for name, K in policies:
         st, ts = M.moe_turnstile_create(K, 0)
         M.check(st, "moe_turnstile_create")
-        waits, lats, make, p_wait, p_enq, rounds = [], [], [], [], [], []
+        waits, iters, marks, p_wait, p_enq, rounds = [], [], [], [], [], []
+        torch.cuda.synchronize()
         t_policy = time.perf_counter()
         prev = d_iteration()
-        t_ready = None
         try:
             for _ in range(args.seg_epochs):
-                t_start = time.perf_counter()
+                p_start = torch.cuda.Event(enable_timing=True)
+                p_start.record(sP)
                 st, runner = M.moe_p_epoch_start(c, ts, epoch, True, T[0], [lg[0]] * L, [xs[0]] * L, [p_out] * L, sP,
                                                  60_000_000)
                 M.check(st, "moe_p_epoch_start")
                 epoch += 1
                 joined = None
                 while True:
-                    prev.synchronize()
-                    now = time.perf_counter()
-                    if t_ready is not None:
-                        lats.append((now - t_ready) * 1e6)
-                    t_ready = now
+                    prev[1].synchronize()  # D is ready once its previous iteration has completed
+                    t_ready = time.perf_counter()
                     M.check(M.moe_turnstile_wait_boundary(ts, 60_000_000), "wait_boundary")
                     done = M.moe_turnstile_query(ts)[1].task == M.MOE_TS_DONE
                     if done:
@@ -420,44 +423,55 @@ def segment_sweep(args, M, c, lg, xs, T, spec, sP, dev):
                             sP.synchronize()
                     waits.append((time.perf_counter() - t_ready) * 1e6)
                     prev = d_iteration()
+                    iters.append(prev)
                     M.check(M.moe_turnstile_release(ts))
                     if done:
                         break
                 st, stats = joined
                 M.check(st, "P epoch")
-                q = M.moe_turnstile_query(ts)[1]
-                rounds.append(q.rounds)
-                sP.synchronize()
-                make.append((time.perf_counter() - t_start) * 1e6)
+                p_end = torch.cuda.Event(enable_timing=True)
+                p_end.record(sP)
+                marks.append((p_start, p_end))
+                rounds.append(M.moe_turnstile_query(ts)[1].rounds)
                 p_wait.append(stats.wait_us)
                 p_enq.append(stats.enqueue_us)
-            prev.synchronize()
-            lats.append((time.perf_counter() - t_ready) * 1e6)
-            t_ready = None
+            # D keeps iterating while the last epoch's P work drains
+            while not marks[-1][1].query():
+                prev[1].synchronize()
+                t_ready = time.perf_counter()
+                M.check(M.moe_turnstile_wait_boundary(ts, 60_000_000), "wait_boundary")
+                waits.append((time.perf_counter() - t_ready) * 1e6)
+                prev = d_iteration()
+                iters.append(prev)
+                M.check(M.moe_turnstile_release(ts))
+            torch.cuda.synchronize()
             wall = time.perf_counter() - t_policy
         finally:
             M.moe_turnstile_destroy(ts)
+        lats = [w + a.elapsed_time(b) * 1e3 for w, (a, b) in zip(waits, iters)]
+        spans = [a.elapsed_time(b) for a, b in marks]
         out[name] = {
             "span": K if name.startswith("fine") else None,
             "d_wait_us_mean": round(sum(waits) / len(waits), 1), "d_wait_us_p99": round(pct(waits, 99), 1),
             "d_iter_us_p50": round(pct(lats, 50), 1), "d_iter_us_p99": round(pct(lats, 99), 1),
-            "d_iters_per_epoch": round(len(waits) / args.seg_epochs, 1),
-            "p_epoch_ms": round(sum(make) / len(make) / 1e3, 3),
+            "d_iters": len(waits),
+            "p_epoch_ms": round(sum(spans) / len(spans), 3),
             "p_wait_for_permit_ms": round(sum(p_wait) / len(p_wait) / 1e3, 3),
             "p_enqueue_ms": round(sum(p_enq) / len(p_enq) / 1e3, 3),
             "rounds_per_epoch": sum(rounds) / len(rounds),
             "wall_ms": round(wall * 1e3, 2),
             "p_layer_tokens_per_s": round(T[0] * L * args.seg_epochs / wall, 1),
-            "d_layer_tokens_per_s": round(T[1] * L * (len(waits) + 1) / wall, 1),
+            "d_layer_tokens_per_s": round(T[1] * L * len(waits) / wall, 1),
         }
         print(f"# segments {name}: {out[name]}", file=sys.stderr, flush=True)
     del graph
     torch.cuda.synchronize()
     return {"layers": L, "epochs_per_policy": args.seg_epochs, "d_iter_alone_us_p50": round(pct(alone, 50), 1),
             "p_epoch_alone_ms": round(min(p_alone) / 1e3, 3), "policies": out,
-            "note": "one P epoch = L layers of the P batch (one boundary per layer, after its dispatch layout); one D "
-                    "iteration = L layers of the D batch replayed as one HIP graph, ready when the previous one "
-                    "completes; D-first admission as in the bench line"}
+            "note": "one P epoch = L layers of the P batch (one boundary per layer, after its dispatch layout), "
+                    "epochs back to back; one D iteration = L layers of the D batch replayed as one HIP graph, ready "
+                    "when the previous one completes, iterating until the last epoch's P work has drained; D-first "
+                    "admission as in the bench line; rates count tokens through one layer"}
 
 
 def main():

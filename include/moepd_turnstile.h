@@ -28,7 +28,7 @@
  *    notification and before routed data movement; the P-epoch runner below
  *    publishes boundary l after moe_dispatch_layout of layer l and moves the
  *    layer's data (moe_dispatch_permute) only once permitted.
- *  - Section 6.3: the segment policy chooses the span; moe_turnstile_set_span
+ *  - Section 6.2: the segment policy chooses the span; moe_turnstile_set_span
  *    changes it between rounds without changing the ordering rules.
  *
  * Conventions
@@ -106,7 +106,7 @@ int moe_turnstile_create(int32_t span, int32_t log_capacity, moe_turnstile_t** o
 /* Free the controller.  No thread may be inside a call on it.  NULL is a no-op. */
 int moe_turnstile_destroy(moe_turnstile_t* ts);
 
-/* Set K for the releases that follow (segment policy, Section 6.3).
+/* Set K for the releases that follow (segment policy, Section 6.2).
  * Errors: MOE_ERR_INVALID_ARG (null, span < 1). */
 int moe_turnstile_set_span(moe_turnstile_t* ts, int32_t span);
 

@@ -85,7 +85,7 @@ def test_rejections():
 
 
 def test_global_enqueue_epoch_takes_one_rendezvous():
-    # Section 7 (ordering ladder): each Global-Enqueue epoch passes one
+    # Section 7.4 (ordering ladder): each Global-Enqueue epoch passes one
     # rendezvous after its 40 dispatch boundaries: with K >= 40 P never stops
     # inside the epoch and D's only entry comes after TaskDone.
     assert O.interior_stops(40, 40) == 0 and O.interior_stops(40, 1000) == 0

@@ -474,6 +474,42 @@ def segment_sweep(args, M, c, lg, xs, T, spec, sP, dev):
                     "admission as in the bench line; rates count tokens through one layer"}
 
 
+def router_measure(M, c, xs, T, spec, inp, sP, sD, bf16, reps=20):
+    """The fused router GEMM (moe_route_from_hidden) of each phase, timed with
+    the per-kernel events: x Wr^T on the matrix cores (float32 partial
+    products over K runs), then the top-k kernel that sums the runs.  Units:
+    2 T E H flops; x (T H) and Wr (E H) in the operand dtype as bytes."""
+    import numpy as np
+    import torch
+
+    from synth import f32_to_bf16_bits
+
+    wt = np.ascontiguousarray(inp.wg.T)
+    w = torch.from_numpy(f32_to_bf16_bits(wt).view(np.int16) if bf16 else wt).to(xs[0].device)
+    esz = 2 if bf16 else 4
+    out = {}
+    streams = {0: sP, 1: sD}
+    M.check(M.moe_timing_enable(c, reps))
+    for ph in (0, 1):
+        for i in range(reps + 2):
+            M.check(M.moe_route_from_hidden(c, ph, xs[ph], w, None, T[ph], streams[ph]), "moe_route_from_hidden")
+            streams[ph].synchronize()
+            M.check(M.moe_phase_reset(c, ph))
+            if i == 1:  # the first two calls are warm-up
+                for kid in range(M.MOE_NUM_KERNELS):
+                    M.moe_timing_read(c, ph, kid)
+        st, ms_g, n_g = M.moe_timing_read(c, ph, M.MOE_KERNEL_ROUTER)
+        st, ms_r, n_r = M.moe_timing_read(c, ph, M.MOE_KERNEL_ROUTE)
+        us_g, us_r = ms_g / max(n_g, 1) * 1e3, ms_r / max(n_r, 1) * 1e3
+        fl = 2.0 * T[ph] * spec.E * spec.H
+        by = (T[ph] + spec.E) * spec.H * esz
+        out["P" if ph == 0 else "D"] = {
+            "tokens": T[ph], "router_gemm_us": round(us_g, 2), "topk_us": round(us_r, 2),
+            "TFLOP/s": round(fl / (us_g * 1e-6) / 1e12, 1), "operand_GB/s": round(by / (us_g * 1e-6) / 1e9, 1)}
+    M.check(M.moe_timing_enable(c, 0))
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -649,6 +685,7 @@ def main():
 
     glat = d_graph_latencies(ctx)
     segments = segment_sweep(args, M, ctx, lg, xs, T, spec, sP, dev) if args.seg_layers > 0 else None
+    router = router_measure(M, ctx_off, xs, T, spec, inp, sP, sD, bf16)
     if ctx_off is not ctx:
         lat_alone_off, _ = d_latencies(False, ctx_off)
         lat_under_off, _ = d_latencies(True, ctx_off)
@@ -718,6 +755,7 @@ def main():
         },
         "roofline": roof,
         "segments": segments,
+        "router_from_hidden": router,
         "kernels": kernels,
         "kernels_pass_ms_per_step": round(wall_events / args.steps * 1e3, 4),
         "kernels_pass_note": "per-kernel HIP events over a second pass of the same concurrent steps, D-first admission "

@@ -78,7 +78,7 @@
 extern "C" {
 #endif
 
-#define MOEPD_ABI_VERSION 1
+#define MOEPD_ABI_VERSION 2
 
 /* Phase ids. */
 enum { MOE_PHASE_P = 0, MOE_PHASE_D = 1, MOE_NUM_PHASES = 2 };
@@ -119,7 +119,8 @@ enum {
   MOE_KERNEL_GEMM1 = 4,   /* grouped gate/up GEMM with fused SwiGLU */
   MOE_KERNEL_GEMM2 = 5,   /* grouped down GEMM */
   MOE_KERNEL_COMBINE = 6, /* weighted gather-combine */
-  MOE_NUM_KERNELS = 7
+  MOE_KERNEL_ROUTER = 7,  /* router GEMM x Wr^T (moe_route_from_hidden) */
+  MOE_NUM_KERNELS = 8
 };
 
 typedef struct moe_config {
@@ -176,6 +177,7 @@ typedef struct moe_phase_view {
   void* x_perm;
   void* h;
   float* y;
+  float* logits; /* [T, E] float32: the logits moe_route_from_hidden selected from */
 } moe_phase_view_t;
 
 typedef struct moe_ctx moe_ctx_t;
@@ -194,6 +196,23 @@ int moe_ctx_create(const moe_config_t* cfg, const moe_weights_t* w, moe_ctx_t** 
  * Errors: MOE_ERR_INVALID_ARG (null ctx; null logits with T > 0; T < 0),
  * MOE_ERR_INVALID_PHASE, MOE_ERR_CAPACITY, MOE_ERR_STATE, MOE_ERR_HIP. */
 int moe_route(moe_ctx_t* ctx, int phase, const float* logits, int32_t T, hipStream_t stream);
+
+/* Gating from hidden states (IDLE -> ROUTED): the router GEMM, then top-k.
+ * logits[t][e] = sum_h x[t][h] w_router[e][h] (+ bias[e]), accumulated in
+ * float32 (bf16 contexts multiply bf16 operands on the matrix cores; float32
+ * contexts use float32 FMAs), stored in the phase's logits buffer
+ * (moe_phase_view: logits); then the top-k gating of moe_route on exactly
+ * those values.  The paper routes each token to its top-k experts (Section
+ * 7.1); the gate's inputs are the token's hidden state.
+ * x: borrowed device [T, H] in the config dtype (the rows moe_dispatch will
+ * move); w_router: borrowed device [E, H] in the config dtype, row e = expert
+ * e's gate vector; bias: borrowed device [E] float32 or NULL.  bf16 contexts
+ * may split the K (hidden) sum into runs added in a fixed order, so results
+ * are deterministic.  Errors: MOE_ERR_INVALID_ARG (null x or w_router with
+ * T > 0, T < 0, null stream), MOE_ERR_INVALID_PHASE, MOE_ERR_CAPACITY,
+ * MOE_ERR_STATE, MOE_ERR_HIP. */
+int moe_route_from_hidden(moe_ctx_t* ctx, int phase, const void* x, const void* w_router, const float* bias,
+                          int32_t T, hipStream_t stream);
 
 /* Dispatch (ROUTED -> DISPATCHED): the notification part computes counts,
  * offsets, row_of_slot and token_of_row (rows of an expert in ascending token

@@ -42,6 +42,7 @@ from __future__ import annotations
 import numpy as np
 
 __all__ = [
+    "router_logits",
     "route",
     "local_map",
     "layout",
@@ -51,6 +52,20 @@ __all__ = [
     "layer",
     "token_output",
 ]
+
+
+def router_logits(x: np.ndarray, w_router: np.ndarray, bias=None) -> np.ndarray:
+    """The gate's logits from hidden states: logits[t, e] = sum_h x[t, h]
+    w_router[e, h] (+ bias[e]), in float64.  x: [T, H]; w_router: [E, H] (row
+    e = expert e's gate vector); bias: [E] or None.  The paper routes tokens
+    to their top-k experts (Section 7.1); the gate reads the token's hidden
+    state through one linear map."""
+    x64 = np.asarray(x, np.float64)
+    w64 = np.asarray(w_router, np.float64)
+    out = x64 @ w64.T
+    if bias is not None:
+        out = out + np.asarray(bias, np.float64)[None, :]
+    return out
 
 
 def route(logits: np.ndarray, k: int):

@@ -42,6 +42,7 @@ struct Phase {
   int nchunks = 1;
   int max_tokens = 0;
   long long rows_cap = 0;
+  int router_cap = 0;  // rows of the router's partial-product buffer
   PhaseBuffers b{};
   void* mem = nullptr;
   hipEvent_t ev = nullptr;
@@ -139,6 +140,11 @@ int alloc_phase(moe_ctx* ctx, int phase) {
   const size_t o_ros = take(slots * 4), o_tor = take(p.rows_cap * 4);
   const size_t o_xp = take(p.rows_cap * c.hidden * ctx->esz), o_h = take(p.rows_cap * c.inter * ctx->esz);
   const size_t o_y = take(p.rows_cap * c.hidden * 4);
+  // Router GEMM: the logits, and room for its K-split partial products (at
+  // least 4096 rows, so that small batches can split K many ways).
+  p.router_cap = c.dtype == MOE_DTYPE_BF16 ? (p.max_tokens > 4096 ? p.max_tokens : 4096) : 0;
+  const size_t o_lg = take((size_t)p.max_tokens * c.num_experts * 4);
+  const size_t o_part = take((size_t)p.router_cap * c.num_experts * 4);
   const size_t o_cc = take((size_t)E * mc * 4), o_tb = take((E + 1) * 4), o_sig = take(4);
 
   void* mem = nullptr;
@@ -160,6 +166,8 @@ int alloc_phase(moe_ctx* ctx, int phase) {
   p.b.chunk_counts = (int32_t*)(base + o_cc);
   p.b.tile_base = (int32_t*)(base + o_tb);
   p.b.signal = (int32_t*)(base + o_sig);
+  p.b.logits = (float*)(base + o_lg);
+  p.b.partials = (float*)(base + o_part);
   // Zero the small metadata (counts, offsets, tile prefix, signal word) once
   // at creation.
   if (hipMemset(base + o_cnt, 0, o_ros - o_cnt) != hipSuccess) return MOE_ERR_HIP;
@@ -314,8 +322,48 @@ int moe_route(moe_ctx_t* ctx, int phase, const float* logits, int32_t T, hipStre
     st = timed(p, MOE_KERNEL_ROUTE, stream,
                [&] {
                  return launch_route(logits, T, c.num_experts, c.top_k, p.b.topk_idx, p.b.topk_w,
-                                     window_of(ctx, phase), stream);
+                                     window_of(ctx, phase), RouterSum{nullptr, nullptr, 1}, stream);
                });
+    if (st) return st;
+  }
+  if ((st = leave(p, stream))) return st;
+  p.T = T;
+  p.state = MOE_STATE_ROUTED;
+  return MOE_OK;
+}
+
+int moe_route_from_hidden(moe_ctx_t* ctx, int phase, const void* x, const void* w_router, const float* bias,
+                          int32_t T, hipStream_t stream) {
+  int st = check_phase(ctx, phase);
+  if (st) return st;
+  if (T < 0 || (T > 0 && (!x || !w_router)) || !stream) return MOE_ERR_INVALID_ARG;
+  Phase& p = ctx->ph[phase];
+  if (p.state != MOE_STATE_IDLE) return MOE_ERR_STATE;
+  if (T > p.max_tokens) return MOE_ERR_CAPACITY;
+  if ((st = enter(ctx, p, stream))) return st;
+  const moe_config_t& c = ctx->cfg;
+  if (T > 0) {
+    int nsplit = 1;
+    if (c.dtype == MOE_DTYPE_BF16) {
+      int ks = 0;
+      nsplit = router_splits(T, c.num_experts, c.hidden, p.router_cap, &ks);
+      float* dst = nsplit > 1 ? p.b.partials : p.b.logits;
+      st = timed(p, MOE_KERNEL_ROUTER, stream, [&] {
+        return launch_router_bf16(x, w_router, T, c.num_experts, c.hidden, dst, nsplit, ks, yield_of(ctx, phase),
+                                  stream);
+      });
+    } else {
+      st = timed(p, MOE_KERNEL_ROUTER, stream, [&] {
+        return launch_router_f32((const float*)x, (const float*)w_router, T, c.num_experts, c.hidden, p.b.logits,
+                                 stream);
+      });
+    }
+    if (st) return st;
+    const float* in = nsplit > 1 ? p.b.partials : p.b.logits;
+    st = timed(p, MOE_KERNEL_ROUTE, stream, [&] {
+      return launch_route(in, T, c.num_experts, c.top_k, p.b.topk_idx, p.b.topk_w, window_of(ctx, phase),
+                          RouterSum{p.b.logits, bias, nsplit}, stream);
+    });
     if (st) return st;
   }
   if ((st = leave(p, stream))) return st;
@@ -433,6 +481,7 @@ int moe_phase_view(const moe_ctx_t* ctx, int phase, moe_phase_view_t* v) {
   v->x_perm = p.b.x_perm;
   v->h = p.b.h;
   v->y = p.b.y;
+  v->logits = p.b.logits;
   return MOE_OK;
 }
 
@@ -535,8 +584,8 @@ int moe_timing_read(moe_ctx_t* ctx, int phase, int kernel, double* total_ms, int
 }
 
 const char* moe_kernel_name(int kernel) {
-  static const char* names[MOE_NUM_KERNELS] = {"route", "count", "place", "permute", "gemm1_swiglu", "gemm2_down",
-                                               "combine"};
+  static const char* names[MOE_NUM_KERNELS] = {"route", "count",   "place",      "permute",
+                                               "gemm1_swiglu", "gemm2_down", "combine", "router_gemm"};
   return (kernel >= 0 && kernel < MOE_NUM_KERNELS) ? names[kernel] : "?";
 }
 

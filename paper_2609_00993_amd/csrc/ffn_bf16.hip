@@ -48,11 +48,30 @@ struct GemmArgs {
   int n_group;    // n-tiles per block of the within-expert tile order (see tile_at)
   int xcd_local;  // 1: consecutive tiles on one XCD (block_tile); 0: dealt round-robin
   YieldTo yield;  // the other phase's layer window to hold back for, if any
+  // Dense mode (the router GEMM): one group of dense_rows rows, no offsets;
+  // K is cut into dense_splits runs of dense_ks slices and split s writes its
+  // partial product to C + s * dense_rows * N.  dense_total = m-tiles x
+  // n-tiles x splits.
+  int dense_rows, dense_splits, dense_ks, dense_total;
 };
 
 struct TileCoord {
   int e, m0, m_end, n0;
+  int split;  // K split of a dense tile (0 otherwise)
 };
+
+// Tile of a dense GEMM: splits outermost, then m-tiles, n-tile fastest (the
+// n-tiles of one row block run side by side and share its activation rows).
+__device__ __forceinline__ void dense_tile_at(const GemmArgs& g, int L, int bm, int bn, TileCoord& tc) {
+  const int per_split = g.dense_total / g.dense_splits;
+  const int s = L / per_split, r = L - s * per_split;
+  const int mt = r / g.n_tiles;
+  tc.e = 0;
+  tc.m0 = mt * bm;
+  tc.m_end = g.dense_rows;
+  tc.n0 = (r - mt * g.n_tiles) * bn;
+  tc.split = s;
+}
 
 // Coordinates of logical tile L.  Tiles run expert-major.  Within an expert
 // (mt m-tiles x n_tiles n-tiles) the n-tiles are cut into blocks of n_group;
@@ -83,6 +102,7 @@ __device__ __forceinline__ void tile_at(const GemmArgs& g, int L, int bm, int bn
   tc.m0 = g.offsets[e] + mt * bm;
   tc.m_end = g.offsets[e + 1];
   tc.n0 = nt * bn;
+  tc.split = 0;
 }
 
 // Logical tile of this workgroup, or -1.  The dispatcher deals workgroups
@@ -90,8 +110,9 @@ __device__ __forceinline__ void tile_at(const GemmArgs& g, int L, int bm, int bn
 // [x per_xcd, (x+1) per_xcd), so the tiles that share an expert's weights
 // run side by side on one XCD's L2.  The grid, a multiple of 8 and at least
 // the largest possible tile count, covers every tile.
+template <bool DENSE = false>
 __device__ __forceinline__ int block_tile(const GemmArgs& g) {
-  const int total = g.tile_base[g.e_loc] * g.n_tiles;
+  const int total = DENSE ? g.dense_total : g.tile_base[g.e_loc] * g.n_tiles;
   if (!g.xcd_local) return (int)blockIdx.x < total ? (int)blockIdx.x : -1;
   const int per_xcd = (total + 7) >> 3;
   const int slot = blockIdx.x >> 3;
@@ -342,7 +363,7 @@ __device__ __forceinline__ void interleave() {
 // index, so the SwiGLU is applied in registers).  The K loop is branch-free:
 // rows past the expert's end are clamped to its last row and discarded at
 // the store, which keeps the MFMA and LDS-read schedule intact.
-template <int BM, int BR, int BK, int WM, int WN, bool GATED, int STAGES>
+template <int BM, int BR, int BK, int WM, int WN, bool GATED, int STAGES, bool DENSE = false>
 __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   constexpr int NB = GATED ? 2 : 1;
   constexpr int BN = BR / NB;
@@ -366,7 +387,8 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / WN, wn = wave % WN;
-  const int KT = g.K / BK;
+  static_assert(!(DENSE && GATED), "the dense mode writes float32 partial products");
+  int KT = g.K / BK;  // slices of this tile (a dense split takes its own run)
   // Per-lane DMA source rows: lane l fills LDS chunk l of its instruction,
   // row r = RPI i + l / CPR, physical chunk l % CPR, so it loads logical
   // chunk (l % CPR) ^ swz(r).
@@ -385,10 +407,12 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
     a_rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(g.A + (size_t)m0 * g.K), (short)0, rows * g.K * 2,
                                                kBufferRsrcWord3);
     const uint16_t* Be = g.B + (size_t)__builtin_amdgcn_readfirstlane(tc.e) * g.b_stride;
+    // first K element of the tile's run (a dense split starts further in)
+    const int k0 = DENSE ? __builtin_amdgcn_readfirstlane(tc.split) * g.dense_ks * BK : 0;
 #pragma unroll
     for (int i = 0; i < A_INS; ++i) {
       const int r = (wave * A_INS + i) * RPI + lrow;
-      a_off[i] = (uint32_t)(r * g.K + (lphys ^ swz<BK>(r)) * 8) * 2u;
+      a_off[i] = (uint32_t)(r * g.K + k0 + (lphys ^ swz<BK>(r)) * 8) * 2u;
     }
 #pragma unroll
     for (int i = 0; i < B_INS; ++i) {
@@ -396,7 +420,7 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
       int brow;
       if (GATED) brow = r < BN ? min(tc.n0 + r, g.N - 1) : g.up_row + min(tc.n0 + r - BN, g.N - 1);
       else brow = min(tc.n0 + r, g.N - 1);
-      b_src[i] = Be + (size_t)brow * g.K + (lphys ^ swz<BK>(r)) * 8;
+      b_src[i] = Be + (size_t)brow * g.K + k0 + (lphys ^ swz<BK>(r)) * 8;
     }
   };
   auto issue = [&](int kt, int slot) {
@@ -448,11 +472,16 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
       for (int j = 0; j < FB; ++j) acc[fm][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[fm], acc[fm][j], 0, 0, 0);
   };
 
-  const int L = block_tile(g);
+  const int L = block_tile<DENSE>(g);
   if (L < 0) return;
   yield_to_window(g.yield);
   TileCoord tc;
-  tile_at(g, L, BM, BN, tc);
+  if constexpr (DENSE) {
+    dense_tile_at(g, L, BM, BN, tc);
+    KT = min(g.dense_ks, KT - tc.split * g.dense_ks);
+  } else {
+    tile_at(g, L, BM, BN, tc);
+  }
   prologue(tc);
 
 #pragma unroll
@@ -518,6 +547,21 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   for (int fm = 0; fm < FM; ++fm) {
     const int row = tc.m0 + wm * WTM + fm * 32 + (lane & 31);
     if (row >= tc.m_end) continue;
+    if constexpr (DENSE) {
+      // partial logits: float32, N (the expert count) need not be a
+      // multiple of 4, so each column is checked
+      float* Cs = static_cast<float*>(g.C) + ((size_t)tc.split * g.dense_rows + row) * g.N;
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int col = tc.n0 + wn * WTN + fn * 32 + 8 * q + 4 * (lane >> 5) + i;
+            if (col < g.N) Cs[col] = acc[fm][fn][4 * q + i];
+          }
+      continue;
+    }
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
 #pragma unroll
@@ -544,6 +588,9 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
 // Distinct entry points so that profiles name each GEMM of each regime.
 __global__ __launch_bounds__(256) void gemm1_swiglu_prefill(GemmArgs g) { gemm_ring_body<128, 256, 64, 2, 2, true, 3>(g); }
 __global__ __launch_bounds__(256) void gemm2_down_prefill(GemmArgs g) { gemm_ring_body<128, 256, 64, 2, 2, false, 3>(g); }
+// The router GEMM: logits = x Wr^T over all T rows, 64 x 128 tiles, K split
+// so that small batches still spread over the GPU.
+__global__ __launch_bounds__(256) void router_gemm(GemmArgs g) { gemm_ring_body<64, 128, 64, 2, 2, false, 3, true>(g); }
 __global__ __launch_bounds__(256) void gemm1_swiglu_wide(GemmArgs g) { gemm_ring_body<256, 256, 32, 2, 2, true, 4>(g); }
 __global__ __launch_bounds__(256) void gemm2_down_wide(GemmArgs g) { gemm_ring_body<256, 256, 32, 2, 2, false, 4>(g); }
 template <bool ROT>
@@ -613,6 +660,49 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
       else gemm2_down_decode<false><<<grid, 256, 0, s>>>(g);
     }
   }
+  return hipGetLastError();
+}
+
+// K splits of the router GEMM: enough tiles x splits to cover the GPU twice,
+// at most 16 splits (the top-k kernel adds them up) and at least 4 slices
+// per split (a split has a three-slice pipeline to fill).
+int router_splits(int T, int E, int H, int cap_rows, int* ks_out) {
+  const int tiles = ((T + 63) / 64) * ((E + 127) / 128);
+  const int kt = H / 64;
+  int s = (512 + tiles - 1) / tiles;
+  s = s < 16 ? s : 16;
+  s = s < kt / 4 ? s : kt / 4;
+  const int by_cap = T > 0 ? cap_rows / T : 1;
+  s = s < by_cap ? s : by_cap;
+  if (s < 1) s = 1;
+  const int ks = (kt + s - 1) / s;
+  *ks_out = ks;
+  return (kt + ks - 1) / ks;
+}
+
+hipError_t launch_router_bf16(const void* x, const void* w, int T, int E, int H, float* out, int splits, int ks,
+                              YieldTo yield, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  GemmArgs g{};
+  g.A = (const uint16_t*)x;
+  g.B = (const uint16_t*)w;
+  g.C = out;
+  g.offsets = nullptr;
+  g.tile_base = nullptr;
+  g.b_stride = 0;
+  g.e_loc = 1;
+  g.N = E;
+  g.K = H;
+  g.up_row = 0;
+  g.n_tiles = (E + 127) / 128;
+  g.n_group = g.n_tiles;
+  g.xcd_local = 0;
+  g.yield = yield;
+  g.dense_rows = T;
+  g.dense_splits = splits;
+  g.dense_ks = ks;
+  g.dense_total = ((T + 63) / 64) * g.n_tiles * splits;
+  router_gemm<<<dim3(round8(g.dense_total)), 256, 0, s>>>(g);
   return hipGetLastError();
 }
 

@@ -156,4 +156,27 @@ hipError_t launch_ffn_f32(int gemm, const PhaseBuffers& b, const void* w_gu, con
   return hipGetLastError();
 }
 
+// Router GEMM of float32 contexts: one wave per token, lane l computes the
+// logits of experts l, l + 64, ... as a sequential float32 FMA chain over h
+// (x[t][h] is the same address for every lane of the wave).
+__global__ __launch_bounds__(256) void router_f32(const float* __restrict__ x, const float* __restrict__ w, int T,
+                                                  int E, int H, float* __restrict__ out) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const int lane = threadIdx.x & 63;
+  const float* xr = x + (size_t)t * H;
+  for (int e = lane; e < E; e += 64) {
+    const float* wr = w + (size_t)e * H;
+    float acc = 0.f;
+    for (int h = 0; h < H; ++h) acc = fmaf(xr[h], wr[h], acc);
+    out[(size_t)t * E + e] = acc;
+  }
+}
+
+hipError_t launch_router_f32(const float* x, const float* w, int T, int E, int H, float* out, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  router_f32<<<dim3((T + 3) / 4), dim3(256), 0, s>>>(x, w, T, E, H, out);
+  return hipGetLastError();
+}
+
 }  // namespace moepd

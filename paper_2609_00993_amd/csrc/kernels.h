@@ -26,6 +26,9 @@ struct PhaseBuffers {
   // layer is between its route and its combine, 0 otherwise.  Written only
   // by this phase's kernels; read by the other phase's grouped GEMMs.
   int32_t* signal;
+  // router GEMM (moe_route_from_hidden)
+  float* logits;    // [Tmax, E] float32, the logits top-k selects from
+  float* partials;  // [router_cap_rows, E] float32, K-split partial products
 };
 
 // A layer window announced to the other phase: the kernels that open and
@@ -57,8 +60,28 @@ inline int dispatch_chunk_tokens(int T, int k, int e_loc) {
   return tc < 1 ? 1 : tc;
 }
 
+// How the route kernel forms its logits after the router GEMM (out == null:
+// read them as given).  logit[t][e] = sum over s < nsplit of
+// in[(s T + t) E + e], in split order, + bias[e] (bias may be null); stored
+// to out[t E + e] (out may equal in when nsplit == 1).
+struct RouterSum {
+  float* out;
+  const float* bias;
+  int nsplit;
+};
+
 hipError_t launch_route(const float* logits, int T, int E, int k, int32_t* topk_idx, float* topk_w,
-                        WindowSignal open, hipStream_t s);
+                        WindowSignal open, RouterSum sum, hipStream_t s);
+
+// Router GEMM (bf16, MFMA): partial logits of T tokens, out[s][t][e] =
+// sum over split s's K run of x[t][h] w[e][h]; x [T, H] and w [E, H] bf16.
+// router_splits picks the split count (and the slices per split, *ks) for a
+// partial buffer of cap_rows rows (splits * T <= cap_rows).
+int router_splits(int T, int E, int H, int cap_rows, int* ks);
+hipError_t launch_router_bf16(const void* x, const void* w, int T, int E, int H, float* out, int splits, int ks,
+                              YieldTo yield, hipStream_t s);
+// Router GEMM (float32, vector ALUs): out[t][e] = sum_h x[t][h] w[e][h].
+hipError_t launch_router_f32(const float* x, const float* w, int T, int E, int H, float* out, hipStream_t s);
 
 // Histogram of each chunk's slots per local expert -> chunk_counts.
 hipError_t launch_count(const int32_t* topk_idx, int T, int k, int e0, int e_loc, int chunk_tokens, int nchunks,

@@ -12,6 +12,10 @@
 // maximum gives the next expert of the ordering, ties included.  The k
 // selections take k shuffle reductions; the selected logit of slot j ends on
 // lane j, which then computes and stores its weight.
+//
+// After the router GEMM the kernel first forms each logit: the sum of the
+// GEMM's K-split partial products in split order, plus the expert's bias if
+// one is given, and stores it (the phase's logits buffer) before selecting.
 #include "common.h"
 #include "kernels.h"
 
@@ -31,9 +35,9 @@ __device__ __forceinline__ float from_orderable(uint32_t o) {
 }
 
 template <int EPL>
-__global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ logits, int T, int E, int k,
+__global__ __launch_bounds__(256) void route_kernel(const float* logits, int T, int E, int k,
                                                     int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
-                                                    WindowSignal open) {
+                                                    WindowSignal open, RouterSum sum) {
   if (open.word && blockIdx.x == 0 && threadIdx.x == 0)
     __hip_atomic_store(open.word, open.gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const int lane = lane_id();
@@ -45,7 +49,29 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     const int e = lane + i * kWave;
-    key[i] = e < E ? ((uint64_t)orderable(row[e]) << 32) | (uint64_t)(0xffffffffu - (uint32_t)e) : 0ull;
+    float v = 0.f;
+    if (e < E) {
+      if (sum.out) {
+        // split order, with eight loads in flight per group of adds
+        const float* p = row + e;
+        const size_t stride = (size_t)T * E;
+        v = p[0];
+        int s = 1;
+        for (; s + 8 <= sum.nsplit; s += 8) {
+          float a[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) a[j] = p[(s + j) * stride];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v += a[j];
+        }
+        for (; s < sum.nsplit; ++s) v += p[s * stride];
+        if (sum.bias) v += sum.bias[e];
+        sum.out[(size_t)t * E + e] = v;
+      } else {
+        v = row[e];
+      }
+    }
+    key[i] = e < E ? ((uint64_t)orderable(v) << 32) | (uint64_t)(0xffffffffu - (uint32_t)e) : 0ull;
   }
 
   float my_l = 0.f, top = 0.f;
@@ -77,19 +103,19 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
 }
 
 hipError_t launch_route(const float* logits, int T, int E, int k, int32_t* topk_idx, float* topk_w,
-                        WindowSignal open, hipStream_t s) {
+                        WindowSignal open, RouterSum sum, hipStream_t s) {
   if (T <= 0) return hipSuccess;
   const dim3 grid((T + 3) / 4), block(256);
   if (E <= 64)
-    route_kernel<1><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open);
+    route_kernel<1><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open, sum);
   else if (E <= 128)
-    route_kernel<2><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open);
+    route_kernel<2><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open, sum);
   else if (E <= 256)
-    route_kernel<4><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open);
+    route_kernel<4><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open, sum);
   else if (E <= 512)
-    route_kernel<8><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open);
+    route_kernel<8><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open, sum);
   else
-    route_kernel<16><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open);
+    route_kernel<16><<<grid, block, 0, s>>>(logits, T, E, k, topk_idx, topk_w, open, sum);
   return hipGetLastError();
 }
 

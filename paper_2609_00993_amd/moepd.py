@@ -48,7 +48,8 @@ MOE_KERNEL_PERMUTE = 3
 MOE_KERNEL_GEMM1 = 4
 MOE_KERNEL_GEMM2 = 5
 MOE_KERNEL_COMBINE = 6
-MOE_NUM_KERNELS = 7
+MOE_KERNEL_ROUTER = 7
+MOE_NUM_KERNELS = 8
 
 
 class moe_config_t(ctypes.Structure):
@@ -85,6 +86,7 @@ class moe_phase_view_t(ctypes.Structure):
         ("x_perm", c_void_p),
         ("h", c_void_p),
         ("y", c_void_p),
+        ("logits", c_void_p),
     ]
 
 
@@ -124,6 +126,7 @@ class moe_p_epoch_stats_t(ctypes.Structure):
 _SIGNATURES = {
     "moe_ctx_create": (c_int, [POINTER(moe_config_t), POINTER(moe_weights_t), POINTER(c_void_p)]),
     "moe_route": (c_int, [c_void_p, c_int, c_void_p, c_int32, c_void_p]),
+    "moe_route_from_hidden": (c_int, [c_void_p, c_int, c_void_p, c_void_p, c_void_p, c_int32, c_void_p]),
     "moe_dispatch": (c_int, [c_void_p, c_int, c_void_p, c_void_p]),
     "moe_dispatch_layout": (c_int, [c_void_p, c_int, c_void_p]),
     "moe_dispatch_permute": (c_int, [c_void_p, c_int, c_void_p, c_void_p]),
@@ -231,6 +234,10 @@ def moe_ctx_create(cfg: moe_config_t, w_gate_up, w_down):
 
 def moe_route(ctx, phase: int, logits, T: int, stream) -> int:
     return _lib.moe_route(ctx, phase, _ptr(logits), T, _stream(stream))
+
+
+def moe_route_from_hidden(ctx, phase: int, x, w_router, bias, T: int, stream) -> int:
+    return _lib.moe_route_from_hidden(ctx, phase, _ptr(x), _ptr(w_router), _ptr(bias), T, _stream(stream))
 
 
 def moe_dispatch(ctx, phase: int, x, stream) -> int:

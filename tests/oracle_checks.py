@@ -30,6 +30,36 @@ def compose_layer(O, logits, x, w_gu, w_dn, k, e0):
                 out=out, x_perm=xp)
 
 
+# ----------------------------------------------------------------------------- router
+
+
+def check_router_bruteforce(O, seed=20):
+    rng = np.random.default_rng(seed)
+    for T, H, E in ((1, 1, 1), (3, 5, 2), (7, 64, 9), (4, 33, 17)):
+        x = rng.standard_normal((T, H))
+        w = rng.standard_normal((E, H))
+        b = rng.standard_normal(E)
+        for bias in (None, b):
+            got = O.router_logits(x, w, bias)
+            assert got.shape == (T, E)
+            for t in range(T):
+                for e in range(E):
+                    ref = math.fsum(float(x[t, h]) * float(w[e, h]) for h in range(H))
+                    if bias is not None:
+                        ref += float(bias[e])
+                    assert abs(got[t, e] - ref) <= 1e-12 * (1 + abs(ref)), (T, H, E, t, e)
+
+
+def check_router_one_hot(O):
+    # x = unit vectors pick columns of the gate matrix: logits[t] = w[:, h_t]
+    H, E = 6, 4
+    w = np.arange(E * H, dtype=np.float64).reshape(E, H) - 7.0
+    x = np.zeros((H, H))
+    x[np.arange(H), np.arange(H)] = 1.0
+    assert np.array_equal(O.router_logits(x, w), w.T)
+    assert np.array_equal(O.router_logits(x, w, np.full(E, 0.5)), w.T + 0.5)
+
+
 # ----------------------------------------------------------------------------- route
 
 
@@ -277,6 +307,8 @@ def check_ep_shares_sum(O, seed=8):
 
 
 ALL_CHECKS = [
+    check_router_bruteforce,
+    check_router_one_hot,
     check_route_bruteforce,
     check_route_argmax,
     check_route_full_order,

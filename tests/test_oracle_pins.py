@@ -13,8 +13,8 @@ from tests import oracle_checks as C
 
 
 def _ns(**override):
-    d = dict(route=M.route, local_map=M.local_map, layout=M.layout, permute=M.permute, expert_ffn=M.expert_ffn,
-             combine=M.combine)
+    d = dict(router_logits=M.router_logits, route=M.route, local_map=M.local_map, layout=M.layout,
+             permute=M.permute, expert_ffn=M.expert_ffn, combine=M.combine)
     d.update(override)
     return types.SimpleNamespace(**d)
 
@@ -155,7 +155,23 @@ def _combine_drop_last(y, w, ros, T, H):
     return M.combine(y, w[:, :-1], ros[:, :-1], T, H)
 
 
+def _router_untransposed(x, w, bias=None):
+    out = np.asarray(x, np.float64) @ np.asarray(w, np.float64).reshape(-1, np.asarray(w).shape[0])
+    return out if bias is None else out + bias
+
+
+def _router_no_bias(x, w, bias=None):
+    return M.router_logits(x, w)
+
+
+def _router_bias_subtracted(x, w, bias=None):
+    return M.router_logits(x, w) - (0 if bias is None else np.asarray(bias, np.float64))
+
+
 MUTANTS = {
+    "router_weights_reshaped_not_transposed": dict(router_logits=_router_untransposed),
+    "router_drops_bias": dict(router_logits=_router_no_bias),
+    "router_bias_subtracted": dict(router_logits=_router_bias_subtracted),
     "route_ties_to_higher_id": dict(route=_route_ties_high),
     "route_no_renormalisation": dict(route=_route_no_renorm),
     "route_signed_zero_ordered": dict(route=_route_signed_zero),

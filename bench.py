@@ -61,6 +61,7 @@ def parse():
     ap.add_argument("--seg-layers", type=int, default=40,
                     help="MoE layers per P epoch and per D iteration in the segment-policy sweep (0: skip it)")
     ap.add_argument("--seg-epochs", type=int, default=2, help="P epochs per policy in the segment-policy sweep")
+    ap.add_argument("--no-router", action="store_true", help="skip the router-GEMM timing")
     ap.add_argument("--d-priority-us", type=int, default=300,
                     help="D-first admission: longest wait of a P GEMM tile for an in-flight D layer (0 = off)")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -685,7 +686,7 @@ def main():
 
     glat = d_graph_latencies(ctx)
     segments = segment_sweep(args, M, ctx, lg, xs, T, spec, sP, dev) if args.seg_layers > 0 else None
-    router = router_measure(M, ctx_off, xs, T, spec, inp, sP, sD, bf16)
+    router = None if args.no_router else router_measure(M, ctx_off, xs, T, spec, inp, sP, sD, bf16)
     if ctx_off is not ctx:
         lat_alone_off, _ = d_latencies(False, ctx_off)
         lat_under_off, _ = d_latencies(True, ctx_off)

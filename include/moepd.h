@@ -39,7 +39,8 @@
  * are ordered by ascending token; expert e computes
  * y = (silu(x W1^T) * (x W3^T)) W2^T; out[t] = sum_j w[t,j] y[row(t,j)]
  * accumulated in float32 in slot order (zero when no slot is resident).
- * The config dtype is the type of the GEMM operands (x, weights, x_perm, h);
+ * The config dtype is the type of the GEMM operands (x, weights, x_perm, h;
+ * for FP8 contexts x is bf16 and the rest MX FP8, see MOE_DTYPE_FP8);
  * y and out are float32, the accumulation precision, in every context.
  *
  * Conventions
@@ -83,8 +84,16 @@ extern "C" {
 /* Phase ids. */
 enum { MOE_PHASE_P = 0, MOE_PHASE_D = 1, MOE_NUM_PHASES = 2 };
 
-/* Element type of x, the weights, x_perm and h (y and out are always float32). */
-enum { MOE_DTYPE_F32 = 0, MOE_DTYPE_BF16 = 1 };
+/* Element type of x, the weights, x_perm and h (y and out are always float32).
+ * MOE_DTYPE_FP8 (Section 7.1 runs FP8 checkpoints; the format is this
+ * library's reading): x is bf16; the weights, x_perm and h are OCP MX FP8 --
+ * E4M3 codes (one byte each) with one E8M0 scale byte per 32 consecutive
+ * values of a row along K (value = E4M3(code) * 2^(scale - 127)).  x_perm and
+ * h are quantized by the kernels: per 32 values of a row, the shared exponent
+ * is floor(log2(max |v|)) - 8 (clamped to [-127, 127]; -127 for an all-zero
+ * block) and each code is v / 2^exponent rounded to nearest even after
+ * clamping to +-448.  H and I must be multiples of 128. */
+enum { MOE_DTYPE_F32 = 0, MOE_DTYPE_BF16 = 1, MOE_DTYPE_FP8 = 2 };
 
 /* Status codes. */
 enum {
@@ -128,9 +137,9 @@ typedef struct moe_config {
   int32_t expert_begin;      /* e0: first resident expert, >= 0 */
   int32_t num_local_experts; /* E_loc: resident experts, 1..256, e0 + E_loc <= E */
   int32_t top_k;             /* k: 1..min(E, 16) */
-  int32_t hidden;            /* H: multiple of 64, 64..16384 */
-  int32_t inter;             /* I: multiple of 64, 64..16384 */
-  int32_t dtype;             /* MOE_DTYPE_F32 or MOE_DTYPE_BF16 */
+  int32_t hidden;            /* H: multiple of 64 (of 128 for FP8), 64..16384 */
+  int32_t inter;             /* I: multiple of 64 (of 128 for FP8), 64..16384 */
+  int32_t dtype;             /* MOE_DTYPE_F32, MOE_DTYPE_BF16 or MOE_DTYPE_FP8 */
   int32_t max_tokens[MOE_NUM_PHASES]; /* capacity per phase, 0..1048576 */
   int32_t flags;             /* must be 0 */
   /* D-first admission, 0..1000 (0 = off).  Section 3.1: ready D work is
@@ -147,10 +156,15 @@ typedef struct moe_config {
  * both phases (row-major, dtype of the config):
  *   w_gate_up [E_loc, 2I, H]: rows [0, I) = W1 (gate), rows [I, 2I) = W3 (up)
  *   w_down    [E_loc, H, I]:  W2
- * They must stay valid for the context's lifetime. */
+ * FP8 contexts pass E4M3 codes there and the E8M0 scale bytes in
+ *   w_gate_up_scales [E_loc, 2I, H / 32], w_down_scales [E_loc, H, I / 32]
+ * (scale b of a row covers its values [32 b, 32 b + 32)); other contexts
+ * pass NULL.  They must stay valid for the context's lifetime. */
 typedef struct moe_weights {
   const void* w_gate_up;
   const void* w_down;
+  const void* w_gate_up_scales;
+  const void* w_down_scales;
 } moe_weights_t;
 
 /* Device pointers and sizes of one phase's owned buffers (read-only for the
@@ -178,6 +192,10 @@ typedef struct moe_phase_view {
   void* h;
   float* y;
   float* logits; /* [T, E] float32: the logits moe_route_from_hidden selected from */
+  /* FP8 contexts: x_perm and h hold E4M3 codes ([R, H], [R, I] bytes) and
+   * these their E8M0 scales ([R, H / 32], [R, I / 32]); NULL otherwise. */
+  uint8_t* x_perm_scales;
+  uint8_t* h_scales;
 } moe_phase_view_t;
 
 typedef struct moe_ctx moe_ctx_t;
@@ -204,8 +222,9 @@ int moe_route(moe_ctx_t* ctx, int phase, const float* logits, int32_t T, hipStre
  * (moe_phase_view: logits); then the top-k gating of moe_route on exactly
  * those values.  The paper routes each token to its top-k experts (Section
  * 7.1); the gate's inputs are the token's hidden state.
- * x: borrowed device [T, H] in the config dtype (the rows moe_dispatch will
- * move); w_router: borrowed device [E, H] in the config dtype, row e = expert
+ * x: borrowed device [T, H] in the config dtype, bf16 for FP8 contexts (the
+ * rows moe_dispatch will move); w_router: borrowed device [E, H] in the same
+ * type (bf16 for FP8 contexts), row e = expert
  * e's gate vector; bias: borrowed device [E] float32 or NULL.  bf16 contexts
  * may split the K (hidden) sum into runs added in a fixed order, so results
  * are deterministic.  Errors: MOE_ERR_INVALID_ARG (null x or w_router with
@@ -217,7 +236,9 @@ int moe_route_from_hidden(moe_ctx_t* ctx, int phase, const void* x, const void* 
 /* Dispatch (ROUTED -> DISPATCHED): the notification part computes counts,
  * offsets, row_of_slot and token_of_row (rows of an expert in ascending token
  * order, no padding); the data part copies x[t] into x_perm[row] for every
- * resident slot.  x: borrowed device [T, H] in the config dtype (T from the
+ * resident slot (FP8 contexts quantize each row to MX FP8 on the way, see
+ * MOE_DTYPE_FP8).  x: borrowed device [T, H] in the config dtype, bf16 for
+ * FP8 contexts (T from the
  * preceding moe_route).  Errors: MOE_ERR_INVALID_ARG (null x with T > 0),
  * MOE_ERR_INVALID_PHASE, MOE_ERR_STATE, MOE_ERR_HIP. */
 int moe_dispatch(moe_ctx_t* ctx, int phase, const void* x, hipStream_t stream);

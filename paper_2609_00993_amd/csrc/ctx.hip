@@ -76,7 +76,9 @@ bool valid_config(const moe_config_t* c) {
   if (c->top_k < 1 || c->top_k > kMaxTopK || c->top_k > c->num_experts) return false;
   if (c->hidden < 64 || c->hidden > 16384 || c->hidden % 64) return false;
   if (c->inter < 64 || c->inter > 16384 || c->inter % 64) return false;
-  if (c->dtype != MOE_DTYPE_F32 && c->dtype != MOE_DTYPE_BF16) return false;
+  if (c->dtype != MOE_DTYPE_F32 && c->dtype != MOE_DTYPE_BF16 && c->dtype != MOE_DTYPE_FP8) return false;
+  // MX FP8 GEMMs step through K 128 values at a time
+  if (c->dtype == MOE_DTYPE_FP8 && (c->hidden % 128 || c->inter % 128)) return false;
   for (int p = 0; p < MOE_NUM_PHASES; ++p)
     if (c->max_tokens[p] < 0 || c->max_tokens[p] > (1 << 20)) return false;
   if (c->flags != 0) return false;
@@ -142,7 +144,7 @@ int alloc_phase(moe_ctx* ctx, int phase) {
   const size_t o_y = take(p.rows_cap * c.hidden * 4);
   // Router GEMM: the logits, and room for its K-split partial products (at
   // least 4096 rows, so that small batches can split K many ways).
-  p.router_cap = c.dtype == MOE_DTYPE_BF16 ? (p.max_tokens > 4096 ? p.max_tokens : 4096) : 0;
+  p.router_cap = c.dtype != MOE_DTYPE_F32 ? (p.max_tokens > 4096 ? p.max_tokens : 4096) : 0;
   const size_t o_lg = take((size_t)p.max_tokens * c.num_experts * 4);
   const size_t o_part = take((size_t)p.router_cap * c.num_experts * 4);
   const size_t o_cc = take((size_t)E * mc * 4), o_tb = take((E + 1) * 4), o_sig = take(4);
@@ -245,13 +247,25 @@ YieldTo yield_of(moe_ctx* ctx, int phase) {
   const Phase& d = ctx->ph[MOE_PHASE_D];
   return YieldTo{d.b.signal, d.gen, (ctx->cfg.d_priority_us * 10 + 33) / 34};
 }
+// MX FP8 contexts keep E4M3 codes and their scale bytes in the x_perm and h
+// regions (sized for bf16 rows, so codes plus scales fit).
+MxBuffers mx_of(const moe_ctx* ctx, const Phase& p) {
+  const size_t R = (size_t)p.rows_cap;
+  uint8_t* xp = static_cast<uint8_t*>(p.b.x_perm);
+  uint8_t* h = static_cast<uint8_t*>(p.b.h);
+  return MxBuffers{xp, xp + R * ctx->cfg.hidden, h, h + R * ctx->cfg.inter};
+}
+
 // Dispatch notification (Section 5.2): the per-chunk histogram, then the
 // prefix sum and stable row assignment.  Picks the phase's tile regime.
 int layout(moe_ctx* ctx, Phase& p, hipStream_t stream) {
   const moe_config_t& c = ctx->cfg;
   const int T = p.T, k = c.top_k, E_loc = c.num_local_experts;
   chunking(T, k, E_loc, &p.chunk_tokens, &p.nchunks);
-  if (c.dtype == MOE_DTYPE_BF16) {
+  if (c.dtype == MOE_DTYPE_FP8) {
+    p.regime = 1;
+    p.bm = ffn_mx_bm();
+  } else if (c.dtype == MOE_DTYPE_BF16) {
     // Rows per resident expert expected under even routing: T*k/E.  Small
     // batches stream weights (32-row tiles); large ones take 128-row tiles,
     // and very large ones 256-row tiles, which move a third fewer bytes into
@@ -275,6 +289,13 @@ int layout(moe_ctx* ctx, Phase& p, hipStream_t stream) {
 // Dispatch data movement: token rows into expert-contiguous rows.
 int permute(moe_ctx* ctx, Phase& p, const void* x, hipStream_t stream) {
   if (p.T == 0) return MOE_OK;
+  if (ctx->cfg.dtype == MOE_DTYPE_FP8) {
+    const MxBuffers mx = mx_of(ctx, p);
+    return timed(p, MOE_KERNEL_PERMUTE, stream, [&] {
+      return launch_permute_mx(x, p.T, ctx->cfg.top_k, ctx->cfg.hidden, p.b.row_of_slot, mx.x_codes, mx.x_scales,
+                               stream);
+    });
+  }
   return timed(p, MOE_KERNEL_PERMUTE, stream, [&] {
     return launch_permute(x, p.T, ctx->cfg.top_k, ctx->cfg.hidden * ctx->esz, p.b.row_of_slot, p.b.x_perm, stream);
   });
@@ -288,11 +309,13 @@ int moe_ctx_create(const moe_config_t* cfg, const moe_weights_t* w, moe_ctx_t** 
   *out = nullptr;
   if (!cfg || !w || !w->w_gate_up || !w->w_down) return MOE_ERR_INVALID_ARG;
   if (!valid_config(cfg)) return MOE_ERR_INVALID_ARG;
+  if (cfg->dtype == MOE_DTYPE_FP8 && (!w->w_gate_up_scales || !w->w_down_scales)) return MOE_ERR_INVALID_ARG;
   moe_ctx* ctx = new (std::nothrow) moe_ctx();
   if (!ctx) return MOE_ERR_OOM;
   ctx->cfg = *cfg;
   ctx->w = *w;
-  ctx->esz = cfg->dtype == MOE_DTYPE_BF16 ? 2 : 4;
+  // bytes of an x element: FP8 contexts take bf16 hidden states
+  ctx->esz = cfg->dtype == MOE_DTYPE_F32 ? 4 : 2;
   if (hipGetDevice(&ctx->device) != hipSuccess) {
     delete ctx;
     return MOE_ERR_HIP;
@@ -344,7 +367,7 @@ int moe_route_from_hidden(moe_ctx_t* ctx, int phase, const void* x, const void* 
   const moe_config_t& c = ctx->cfg;
   if (T > 0) {
     int nsplit = 1;
-    if (c.dtype == MOE_DTYPE_BF16) {
+    if (c.dtype != MOE_DTYPE_F32) {
       int ks = 0;
       nsplit = router_splits(T, c.num_experts, c.hidden, p.router_cap, &ks);
       float* dst = nsplit > 1 ? p.b.partials : p.b.logits;
@@ -428,6 +451,10 @@ int moe_expert_ffn(moe_ctx_t* ctx, int phase, hipStream_t stream) {
     const int max_m_tiles = (int)((rows + p.bm - 1) / p.bm) + c.num_local_experts;
     for (int gemm = 1; gemm <= 2; ++gemm) {
       st = timed(p, gemm == 1 ? MOE_KERNEL_GEMM1 : MOE_KERNEL_GEMM2, stream, [&] {
+        if (c.dtype == MOE_DTYPE_FP8)
+          return launch_ffn_mx(gemm, p.b, mx_of(ctx, p),
+                               MxWeights{ctx->w.w_gate_up, ctx->w.w_gate_up_scales, ctx->w.w_down, ctx->w.w_down_scales},
+                               c.num_local_experts, c.hidden, c.inter, max_m_tiles, yield_of(ctx, phase), stream);
         if (c.dtype == MOE_DTYPE_BF16)
           return launch_ffn_bf16(p.regime, gemm, p.b, ctx->w.w_gate_up, ctx->w.w_down, c.num_local_experts, c.hidden,
                                  c.inter, max_m_tiles, yield_of(ctx, phase), stream);
@@ -482,6 +509,11 @@ int moe_phase_view(const moe_ctx_t* ctx, int phase, moe_phase_view_t* v) {
   v->h = p.b.h;
   v->y = p.b.y;
   v->logits = p.b.logits;
+  if (ctx->cfg.dtype == MOE_DTYPE_FP8) {
+    const MxBuffers mx = mx_of(ctx, p);
+    v->x_perm_scales = mx.x_scales;
+    v->h_scales = mx.h_scales;
+  }
   return MOE_OK;
 }
 

@@ -109,6 +109,27 @@ int ffn_bf16_bm(int regime);
 hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
                            int e_loc, int H, int I, int max_m_tiles, YieldTo yield, hipStream_t s);
 
+// MX FP8 contexts: the phase's x_perm and h regions hold E4M3 codes
+// followed by their E8M0 scale bytes (one per 32 values of a row).
+struct MxBuffers {
+  uint8_t* x_codes;   // [Rcap, H]
+  uint8_t* x_scales;  // [Rcap, H / 32]
+  uint8_t* h_codes;   // [Rcap, I]
+  uint8_t* h_scales;  // [Rcap, I / 32]
+};
+struct MxWeights {
+  const void* gu;         // [E_loc, 2I, H] E4M3 codes
+  const void* gu_scales;  // [E_loc, 2I, H / 32] E8M0
+  const void* dn;         // [E_loc, H, I] E4M3 codes
+  const void* dn_scales;  // [E_loc, H, I / 32] E8M0
+};
+// x (bf16 rows) -> MX FP8 codes and scales of every resident row.
+hipError_t launch_permute_mx(const void* x, int T, int k, int H, const int32_t* row_of_slot, uint8_t* codes,
+                             uint8_t* scales, hipStream_t s);
+int ffn_mx_bm();
+hipError_t launch_ffn_mx(int gemm, const PhaseBuffers& b, const MxBuffers& mx, const MxWeights& w, int e_loc, int H,
+                         int I, int max_m_tiles, YieldTo yield, hipStream_t s);
+
 int ffn_f32_bm();
 hipError_t launch_ffn_f32(int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn, int e_loc, int H,
                           int I, int max_m_tiles, hipStream_t s);

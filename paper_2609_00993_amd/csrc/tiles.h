@@ -1,0 +1,99 @@
+// Tile scheduling shared by the grouped GEMMs (bf16 and MX FP8): logical
+// tile ids, their (expert, row block, column block) coordinates, and the
+// XCD-aware mapping of workgroups to tiles.  G is a GEMM argument struct
+// with offsets, tile_base, e_loc, n_tiles, n_group and xcd_local (and the
+// dense_* fields for the dense mode).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace moepd {
+
+struct TileCoord {
+  int e, m0, m_end, n0;
+  int split;  // K split of a dense tile (0 otherwise)
+};
+
+// Tile of a dense GEMM: splits outermost, then m-tiles, n-tile fastest (the
+// n-tiles of one row block run side by side and share its activation rows).
+template <class G>
+__device__ __forceinline__ void dense_tile_at(const G& g, int L, int bm, int bn, TileCoord& tc) {
+  const int per_split = g.dense_total / g.dense_splits;
+  const int s = L / per_split, r = L - s * per_split;
+  const int mt = r / g.n_tiles;
+  tc.e = 0;
+  tc.m0 = mt * bm;
+  tc.m_end = g.dense_rows;
+  tc.n0 = (r - mt * g.n_tiles) * bn;
+  tc.split = s;
+}
+
+// Coordinates of logical tile L.  Tiles run expert-major.  Within an expert
+// (mt m-tiles x n_tiles n-tiles) the n-tiles are cut into blocks of n_group;
+// block by block, the tiles go m-tile by m-tile, n-tile fastest.  So
+// consecutive tiles (which one XCD runs side by side, see block_tile) share
+// an activation row block across n_group n-tiles and a weight n-tile across
+// the m-tiles running together.  n_group = n_tiles is plain m-major order.
+template <class G>
+__device__ __forceinline__ void tile_at(const G& g, int L, int bm, int bn, TileCoord& tc) {
+  int lo = 0, hi = g.e_loc - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (g.tile_base[mid] * g.n_tiles <= L) lo = mid;
+    else hi = mid - 1;
+  }
+  const int e = lo;
+  const int mt_e = g.tile_base[e + 1] - g.tile_base[e];
+  const int local = L - g.tile_base[e] * g.n_tiles;
+  const int b = g.n_group;
+  const int full = g.n_tiles / b;  // full n-blocks; a narrower one may follow
+  int blk = local / (mt_e * b), bw = b, r;
+  if (blk >= full) {
+    blk = full;
+    bw = g.n_tiles - full * b;
+  }
+  r = local - blk * mt_e * b;
+  const int mt = r / bw, nt = blk * b + (r - mt * bw);
+  tc.e = e;
+  tc.m0 = g.offsets[e] + mt * bm;
+  tc.m_end = g.offsets[e + 1];
+  tc.n0 = nt * bn;
+  tc.split = 0;
+}
+
+// Logical tile of this workgroup, or -1.  The dispatcher deals workgroups
+// round-robin to the 8 XCDs; XCD x takes the logical tiles
+// [x per_xcd, (x+1) per_xcd), so the tiles that share an expert's weights
+// run side by side on one XCD's L2.  The grid, a multiple of 8 and at least
+// the largest possible tile count, covers every tile.
+template <bool DENSE = false, class G>
+__device__ __forceinline__ int block_tile(const G& g) {
+  int total;
+  if constexpr (DENSE) total = g.dense_total;
+  else total = g.tile_base[g.e_loc] * g.n_tiles;
+  if (!g.xcd_local) return (int)blockIdx.x < total ? (int)blockIdx.x : -1;
+  const int per_xcd = (total + 7) >> 3;
+  const int slot = blockIdx.x >> 3;
+  if (slot >= per_xcd) return -1;
+  const int L = (blockIdx.x & 7) * per_xcd + slot;
+  return L < total ? L : -1;
+}
+
+// D first (Section 3.1): the planner admits ready D work before P, and a
+// long P execution is cut into segments so that D advances between them
+// (Section 4.2).  On one GPU the segment is a GEMM tile: while the other
+// phase's layer window is open, a workgroup about to start a tile sleeps in
+// steps of 127 * 64 cycles until the window closes, at most `polls` times.
+// The wait is bounded, so the kernel always finishes, and it is only a hint:
+// no result depends on it.
+__device__ __forceinline__ void yield_to_window(const YieldTo& y) {
+  if (!y.word) return;
+  for (int i = 0; i < y.polls; ++i) {
+    if (__hip_atomic_load(y.word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != y.gen) return;
+    __builtin_amdgcn_s_sleep(127);
+  }
+}
+
+}  // namespace moepd

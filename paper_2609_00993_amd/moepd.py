@@ -23,7 +23,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libmoepd.so")
 
 MOE_PHASE_P, MOE_PHASE_D, MOE_NUM_PHASES = 0, 1, 2
-MOE_DTYPE_F32, MOE_DTYPE_BF16 = 0, 1
+MOE_DTYPE_F32, MOE_DTYPE_BF16, MOE_DTYPE_FP8 = 0, 1, 2
 
 MOE_OK = 0
 MOE_ERR_INVALID_ARG = -1
@@ -68,7 +68,8 @@ class moe_config_t(ctypes.Structure):
 
 
 class moe_weights_t(ctypes.Structure):
-    _fields_ = [("w_gate_up", c_void_p), ("w_down", c_void_p)]
+    _fields_ = [("w_gate_up", c_void_p), ("w_down", c_void_p), ("w_gate_up_scales", c_void_p),
+                ("w_down_scales", c_void_p)]
 
 
 class moe_phase_view_t(ctypes.Structure):
@@ -87,6 +88,8 @@ class moe_phase_view_t(ctypes.Structure):
         ("h", c_void_p),
         ("y", c_void_p),
         ("logits", c_void_p),
+        ("x_perm_scales", c_void_p),
+        ("h_scales", c_void_p),
     ]
 
 
@@ -225,8 +228,8 @@ def make_config(num_experts, expert_begin, num_local_experts, top_k, hidden, int
     return c
 
 
-def moe_ctx_create(cfg: moe_config_t, w_gate_up, w_down):
-    w = moe_weights_t(_ptr(w_gate_up), _ptr(w_down))
+def moe_ctx_create(cfg: moe_config_t, w_gate_up, w_down, w_gate_up_scales=None, w_down_scales=None):
+    w = moe_weights_t(_ptr(w_gate_up), _ptr(w_down), _ptr(w_gate_up_scales), _ptr(w_down_scales))
     out = c_void_p()
     st = _lib.moe_ctx_create(byref(cfg) if cfg is not None else None, byref(w), byref(out))
     return st, out.value

@@ -4,6 +4,7 @@ from .gen import (
     BF16,
     CONFIGS,
     F32,
+    FP8,
     LayerInputs,
     LayerSpec,
     TraceStep,
@@ -21,6 +22,7 @@ __all__ = [
     "BF16",
     "CONFIGS",
     "F32",
+    "FP8",
     "LayerInputs",
     "LayerSpec",
     "TraceStep",

@@ -17,6 +17,13 @@ nearest even) and keep the bit patterns; logits are the float32 rounding of
 the float64 product of the (rounded) hidden rows with Wg, plus a per-expert
 bias for skewed routing.  The logits are an input of the routing call, so
 the oracle and the GPU see the very same float32 values.
+
+FP8 workloads keep bf16 hidden rows and draw the expert weights directly in
+OCP MX FP8: each block's standard normals times 16 become E4M3 codes
+(PyTorch's float8_e4m3fn conversion), and each row's 32-value groups get an
+E8M0 scale byte 127 + round(log2(std / 16)) + j with j drawn uniformly from
+{-1, 0, 1} (so several scales occur), from the same stream.  The float32
+values are the codes' values times their scales (exact).
 """
 
 from __future__ import annotations
@@ -31,6 +38,7 @@ import numpy as np
 
 F32 = "f32"
 BF16 = "bf16"
+FP8 = "fp8"
 
 
 @dataclasses.dataclass(frozen=True)
@@ -44,7 +52,7 @@ class LayerSpec:
     k: int  # top-k
     H: int  # hidden size
     I: int  # FFN intermediate size
-    dtype: str  # "f32" or "bf16"
+    dtype: str  # "f32", "bf16" or "fp8" (MX FP8 weights, bf16 hidden rows)
     T_P: int  # prefill batch tokens
     T_D: int  # decode batch tokens
     zipf_s: Optional[float] = None  # skewed routing exponent (None = uniform-ish)
@@ -65,6 +73,13 @@ CONFIGS = {
     # here are the token pools the trace's batches are windows of
     4: LayerSpec("dsv3-share-agentic-bf16", E=256, e0=0, E_loc=32, k=8, H=7168, I=2048, dtype=BF16, T_P=16384,
                  T_D=256),
+    # the config-2 share with MX FP8 expert weights
+    5: LayerSpec("dsv3-share-fp8", E=256, e0=0, E_loc=32, k=8, H=7168, I=2048, dtype=FP8, T_P=8192, T_D=128),
+    # the paper's own model shape (hidden 2560, 512 routed experts, top-8)
+    # at one GPU's share of EP8 (64 resident); the expert width I = 768 is a
+    # reading (the paper does not state it)
+    6: LayerSpec("paper-shape-fp8", E=512, e0=0, E_loc=64, k=8, H=2560, I=768, dtype=FP8, T_P=8192, T_D=256),
+    7: LayerSpec("paper-shape-bf16", E=512, e0=0, E_loc=64, k=8, H=2560, I=768, dtype=BF16, T_P=8192, T_D=256),
 }
 
 
@@ -102,13 +117,31 @@ class LayerInputs:
     w_dn: np.ndarray  # [E_loc, H, I] f32 values
     x: dict  # phase -> [T, H] f32 values
     logits: dict  # phase -> [T, E] f32
-    w_gu_bits: Optional[np.ndarray] = None
+    w_gu_bits: Optional[np.ndarray] = None  # bf16 bits, or E4M3 codes (uint8) for fp8
     w_dn_bits: Optional[np.ndarray] = None
     x_bits: Optional[dict] = None
+    w_gu_scales: Optional[np.ndarray] = None  # fp8: E8M0 bytes [E_loc, 2I, H / 32]
+    w_dn_scales: Optional[np.ndarray] = None  # fp8: E8M0 bytes [E_loc, H, I / 32]
 
 
 def _stream(seed: int, block: int) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, block])))
+
+
+def _draw_mx_block(seed: int, block: int, shape, std: float):
+    """One MX FP8 weight block (see the module recipe).  Returns (float32
+    values, E4M3 codes uint8, E8M0 scales uint8 [..., K / 32])."""
+    import torch
+
+    rng = _stream(seed, block)
+    a = rng.standard_normal(size=shape, dtype=np.float32) * np.float32(16.0)
+    codes = torch.from_numpy(a).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    base = 127 + int(round(math.log2(std / 16.0)))
+    sshape = tuple(shape[:-1]) + (shape[-1] // 32,)
+    scales = (base + rng.integers(-1, 2, size=sshape)).astype(np.uint8)
+    vals = torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float32).numpy()
+    vals = (vals.reshape(sshape + (32,)) * np.exp2(scales.astype(np.float32) - 127)[..., None]).reshape(shape)
+    return vals.astype(np.float32), codes, scales
 
 
 def _draw_block(seed: int, block: int, shape, std: float, dtype: str):
@@ -140,13 +173,25 @@ def make_layer(spec: LayerSpec, seed: int, bias: Optional[np.ndarray] = None) ->
     H, I, E, E_loc = spec.H, spec.I, spec.E, spec.E_loc
     wstd = 1.0 / math.sqrt(H)
     bf16 = spec.dtype == BF16
+    fp8 = spec.dtype == FP8
     w_gu = np.empty((E_loc, 2 * I, H), np.float32)
     w_dn = np.empty((E_loc, H, I), np.float32)
     w_gu_bits = np.empty((E_loc, 2 * I, H), np.uint16) if bf16 else None
     w_dn_bits = np.empty((E_loc, H, I), np.uint16) if bf16 else None
+    if fp8:
+        w_gu_bits = np.empty((E_loc, 2 * I, H), np.uint8)
+        w_dn_bits = np.empty((E_loc, H, I), np.uint8)
+        w_gu_scales = np.empty((E_loc, 2 * I, H // 32), np.uint8)
+        w_dn_scales = np.empty((E_loc, H, I // 32), np.uint8)
 
     def expert(job):
         kind, e = job
+        if fp8:
+            if kind == "gu":
+                w_gu[e], w_gu_bits[e], w_gu_scales[e] = _draw_mx_block(seed, 1 + e, (2 * I, H), wstd)
+            else:
+                w_dn[e], w_dn_bits[e], w_dn_scales[e] = _draw_mx_block(seed, 1 + E_loc + e, (H, I), wstd)
+            return
         if kind == "gu":
             v, b = _draw_block(seed, 1 + e, (2 * I, H), wstd, spec.dtype)
             w_gu[e] = v
@@ -161,7 +206,8 @@ def make_layer(spec: LayerSpec, seed: int, bias: Optional[np.ndarray] = None) ->
     jobs = [("gu", e) for e in range(E_loc)] + [("dn", e) for e in range(E_loc)]
     with cf.ThreadPoolExecutor(_POOL_WORKERS) as ex:
         list(ex.map(expert, jobs))
-        fx = {ph: ex.submit(_draw_block, seed, 2 * E_loc + 1 + ph, ((spec.T_P, spec.T_D)[ph], H), 1.0, spec.dtype)
+        xdt = BF16 if fp8 else spec.dtype  # FP8 layers take bf16 hidden rows
+        fx = {ph: ex.submit(_draw_block, seed, 2 * E_loc + 1 + ph, ((spec.T_P, spec.T_D)[ph], H), 1.0, xdt)
               for ph in (0, 1)}
         wg = _stream(seed, 0).standard_normal(size=(H, E), dtype=np.float32) * np.float32(wstd)
         x, x_bits = {}, {}
@@ -181,7 +227,9 @@ def make_layer(spec: LayerSpec, seed: int, bias: Optional[np.ndarray] = None) ->
         logits=logits,
         w_gu_bits=w_gu_bits,
         w_dn_bits=w_dn_bits,
-        x_bits=x_bits if bf16 else None,
+        x_bits=x_bits if (bf16 or fp8) else None,
+        w_gu_scales=w_gu_scales if fp8 else None,
+        w_dn_scales=w_dn_scales if fp8 else None,
     )
 
 

@@ -8,7 +8,7 @@ import math
 
 import numpy as np
 
-from synth import BF16, bf16_bits_to_f32
+from synth import BF16, FP8, bf16_bits_to_f32
 
 _hip = None
 
@@ -65,18 +65,22 @@ class GpuLayer:
         spec = inp.spec
         self.spec = spec
         self.bf16 = spec.dtype == BF16
+        self.fp8 = spec.dtype == FP8
         self.T = {0: spec.T_P, 1: spec.T_D}
         if max_tokens is None:
             max_tokens = (spec.T_P, spec.T_D)
-        self.w_gu = to_dev(inp.w_gu_bits if self.bf16 else inp.w_gu)
-        self.w_dn = to_dev(inp.w_dn_bits if self.bf16 else inp.w_dn)
-        self.x = {ph: to_dev(inp.x_bits[ph] if self.bf16 else inp.x[ph]) for ph in (0, 1)}
+        packed = self.bf16 or self.fp8  # weights as bit patterns / codes
+        self.w_gu = to_dev(inp.w_gu_bits if packed else inp.w_gu)
+        self.w_dn = to_dev(inp.w_dn_bits if packed else inp.w_dn)
+        self.w_gu_s = to_dev(inp.w_gu_scales) if self.fp8 else None
+        self.w_dn_s = to_dev(inp.w_dn_scales) if self.fp8 else None
+        self.x = {ph: to_dev(inp.x_bits[ph] if packed else inp.x[ph]) for ph in (0, 1)}
         self.logits = {ph: to_dev(inp.logits[ph]) for ph in (0, 1)}
         self.out = {ph: torch.zeros((self.T[ph], spec.H), dtype=torch.float32, device="cuda") for ph in (0, 1)}
-        cfg = M.make_config(spec.E, spec.e0, spec.E_loc, spec.k, spec.H, spec.I,
-                            M.MOE_DTYPE_BF16 if self.bf16 else M.MOE_DTYPE_F32, max_tokens[0], max_tokens[1],
+        dt = M.MOE_DTYPE_FP8 if self.fp8 else M.MOE_DTYPE_BF16 if self.bf16 else M.MOE_DTYPE_F32
+        cfg = M.make_config(spec.E, spec.e0, spec.E_loc, spec.k, spec.H, spec.I, dt, max_tokens[0], max_tokens[1],
                             d_priority_us=d_priority_us)
-        st, self.ctx = M.moe_ctx_create(cfg, self.w_gu, self.w_dn)
+        st, self.ctx = M.moe_ctx_create(cfg, self.w_gu, self.w_dn, self.w_gu_s, self.w_dn_s)
         if st == M.MOE_ERR_HIP:
             err = hip_last_error()
             raise AssertionError(f"moe_ctx_create: HIP error {err} (free/total {torch.cuda.mem_get_info()})")
@@ -106,11 +110,17 @@ class GpuLayer:
         R = int(res["offsets"][-1])
         res["R"] = R
         res["token_of_row"] = read_dev(v.token_of_row, (R,), np.int32)
+        res["y"] = read_dev(v.y, (R, spec.H), np.float32)
+        res["out"] = self.out[ph].cpu().numpy()
+        if self.fp8:
+            res["x_codes"] = read_dev(v.x_perm, (R, spec.H), np.uint8)
+            res["x_scales"] = read_dev(v.x_perm_scales, (R, spec.H // 32), np.uint8)
+            res["h_codes"] = read_dev(v.h, (R, spec.I), np.uint8)
+            res["h_scales"] = read_dev(v.h_scales, (R, spec.I // 32), np.uint8)
+            return res
         edt = np.uint16 if self.bf16 else np.float32
         res["x_perm_raw"] = read_dev(v.x_perm, (R, spec.H), edt)
         res["h_raw"] = read_dev(v.h, (R, spec.I), edt)
-        res["y"] = read_dev(v.y, (R, spec.H), np.float32)
-        res["out"] = self.out[ph].cpu().numpy()
         for key in ("x_perm", "h"):
             raw = res[key + "_raw"]
             res[key] = bf16_bits_to_f32(raw) if self.bf16 else raw

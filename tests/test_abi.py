@@ -72,6 +72,19 @@ def test_create_rejects_bad_config_without_gpu(lib, bad):
     assert st == lib.MOE_ERR_INVALID_ARG and ctx is None
 
 
+def test_fp8_create_validation_without_gpu(lib):
+    # MX FP8 steps through K 128 at a time; its weights carry scale arrays
+    st, ctx = lib.moe_ctx_create(_cfg(lib, dtype=lib.MOE_DTYPE_FP8, hidden=192, inter=256), 0x1000, 0x2000, 0x3000,
+                                 0x4000)
+    assert st == lib.MOE_ERR_INVALID_ARG and ctx is None
+    st, ctx = lib.moe_ctx_create(_cfg(lib, dtype=lib.MOE_DTYPE_FP8, hidden=256, inter=192), 0x1000, 0x2000, 0x3000,
+                                 0x4000)
+    assert st == lib.MOE_ERR_INVALID_ARG and ctx is None
+    st, ctx = lib.moe_ctx_create(_cfg(lib, dtype=lib.MOE_DTYPE_FP8, hidden=256, inter=256), 0x1000, 0x2000, None,
+                                 0x4000)
+    assert st == lib.MOE_ERR_INVALID_ARG and ctx is None
+
+
 def test_create_rejects_null_weights(lib):
     st, ctx = lib.moe_ctx_create(_cfg(lib), 0, 0x2000)
     assert st == lib.MOE_ERR_INVALID_ARG and ctx is None

@@ -42,6 +42,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak, TFLOP/s
+MFMA_FP8_PEAK_TFLOPS = 5000.0  # dense fp8 matrix-core peak, TFLOP/s
 FP32_VECTOR_PEAK_TFLOPS = 157.3
 
 METRIC = "MoE-layer tokens/s (P+D concurrent, 1 GPU); D-layer p50 latency under P load"
@@ -53,7 +54,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=1,
-                    help="workload id (0..4); 1 is the headline workload, 4 the agentic trace on the config-2 layer")
+                    help="workload id (0..7); 1 is the headline workload, 4 the agentic trace on the config-2 layer, "
+                         "5 the config-2 layer in MX FP8, 6/7 the paper's model shape in FP8/BF16")
     ap.add_argument("--trace-steps", type=int, default=200, help="steps of the agentic trace (config 4)")
     ap.add_argument("--d-iters", type=int, default=60, help="D layers per latency measurement")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
@@ -84,21 +86,24 @@ def workload_name(spec):
             f"SwiGLU {spec.dtype}{skew}, P {spec.T_P} + D {spec.T_D} tokens concurrent on two streams")
 
 
-def kernel_units(spec, kernel, T, R, touched, esz):
+def kernel_units(spec, kernel, T, R, touched, esz, osz=None):
     """(algorithmic bytes, algorithmic flops) of one launch of `kernel` for a
-    phase batch of T tokens with R resident rows over `touched` experts."""
+    phase batch of T tokens with R resident rows over `touched` experts.
+    esz: bytes of an x element; osz: bytes per element of the GEMM operands
+    (weights, x_perm, h), scales included (1 + 1/32 for MX FP8)."""
     H, I, E, k = spec.H, spec.I, spec.E, spec.k
+    osz = esz if osz is None else osz
     if kernel == "route":
         return T * E * 4 + T * k * 8, 0
     if kernel in ("count", "place"):
         return T * k * 4 * (1 if kernel == "count" else 2) + R * 4, 0
     if kernel == "permute":
         tokens_touched = T  # every token row is read once (tokens with no resident slot too)
-        return (tokens_touched + R) * H * esz, 0
+        return int(tokens_touched * H * esz + R * H * osz), 0
     if kernel == "gemm1_swiglu":
-        return touched * 2 * I * H * esz + R * H * esz + R * I * esz, 4 * R * H * I
+        return int(touched * 2 * I * H * osz + R * H * osz + R * I * osz), 4 * R * H * I
     if kernel == "gemm2_down":
-        return touched * H * I * esz + R * I * esz + R * H * 4, 2 * R * H * I
+        return int(touched * H * I * osz + R * I * osz + R * H * 4), 2 * R * H * I
     if kernel == "combine":
         return R * H * 4 + T * H * 4 + T * k * 8, 0
     return 0, 0
@@ -130,9 +135,16 @@ def cpu_baseline(inp, seconds):
     cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     tokens, reps = 0, 0
     t0 = time.perf_counter()
+    fp8 = inp.w_gu_scales is not None
+    if fp8:
+        from oracle import mx as oracle_mx
     while True:
         for ph in (0, 1):
-            oracle.layer(inp.logits[ph], inp.x[ph], inp.w_gu, inp.w_dn, spec.k, spec.e0)
+            if fp8:
+                oracle_mx.layer_mx(inp.logits[ph], inp.x[ph], inp.w_gu_bits, inp.w_gu_scales, inp.w_dn_bits,
+                                   inp.w_dn_scales, spec.k, spec.e0)
+            else:
+                oracle.layer(inp.logits[ph], inp.x[ph], inp.w_gu, inp.w_dn, spec.k, spec.e0)
             tokens += (spec.T_P, spec.T_D)[ph]
         reps += 1
         el = time.perf_counter() - t0
@@ -151,7 +163,7 @@ def cpu_baseline(inp, seconds):
         "cores": int(threads),
         "kind": "oracle",
         "sample": f"{reps} full P ({spec.T_P}) + D ({spec.T_D}) layer passes of the same workload, float64 numpy "
-                  f"oracle, {el:.1f} s",
+                  f"oracle{' (MX FP8)' if fp8 else ''}, {el:.1f} s",
     }
 
 
@@ -522,7 +534,7 @@ def main():
     import torch
 
     from paper_2609_00993_amd import moepd as M
-    from synth import BF16, make_config
+    from synth import BF16, FP8, make_config
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -537,22 +549,29 @@ def main():
         return
     spec = inp.spec
     bf16 = spec.dtype == BF16
-    esz = 2 if bf16 else 4
+    fp8 = spec.dtype == FP8
+    packed = bf16 or fp8
+    esz = 2 if packed else 4  # bytes of an x element
+    osz = 1 + 1 / 32 if fp8 else esz  # bytes per GEMM operand element, scales included
+    mma_peak = MFMA_FP8_PEAK_TFLOPS if fp8 else MFMA_BF16_PEAK_TFLOPS
 
     def up(a):
         a = np.ascontiguousarray(a)
         return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to(dev)
 
-    w_gu = up(inp.w_gu_bits if bf16 else inp.w_gu)
-    w_dn = up(inp.w_dn_bits if bf16 else inp.w_dn)
-    xs = {ph: up(inp.x_bits[ph] if bf16 else inp.x[ph]) for ph in (0, 1)}
+    w_gu = up(inp.w_gu_bits if packed else inp.w_gu)
+    w_dn = up(inp.w_dn_bits if packed else inp.w_dn)
+    w_gu_s = up(inp.w_gu_scales) if fp8 else None
+    w_dn_s = up(inp.w_dn_scales) if fp8 else None
+    xs = {ph: up(inp.x_bits[ph] if packed else inp.x[ph]) for ph in (0, 1)}
     lg = {ph: up(inp.logits[ph]) for ph in (0, 1)}
     T = {0: spec.T_P, 1: spec.T_D}
     outs = {ph: torch.empty((T[ph], spec.H), dtype=torch.float32, device=dev) for ph in (0, 1)}
     def make_ctx(d_priority_us):
         cfg = M.make_config(spec.E, spec.e0, spec.E_loc, spec.k, spec.H, spec.I,
-                            M.MOE_DTYPE_BF16 if bf16 else M.MOE_DTYPE_F32, T[0], T[1], d_priority_us=d_priority_us)
-        st, c = M.moe_ctx_create(cfg, w_gu, w_dn)
+                            M.MOE_DTYPE_FP8 if fp8 else M.MOE_DTYPE_BF16 if bf16 else M.MOE_DTYPE_F32, T[0], T[1],
+                            d_priority_us=d_priority_us)
+        st, c = M.moe_ctx_create(cfg, w_gu, w_dn, w_gu_s, w_dn_s)
         M.check(st, "moe_ctx_create")
         return c
 
@@ -686,7 +705,7 @@ def main():
 
     glat = d_graph_latencies(ctx)
     segments = segment_sweep(args, M, ctx, lg, xs, T, spec, sP, dev) if args.seg_layers > 0 else None
-    router = None if args.no_router else router_measure(M, ctx_off, xs, T, spec, inp, sP, sD, bf16)
+    router = None if args.no_router else router_measure(M, ctx_off, xs, T, spec, inp, sP, sD, packed)
     if ctx_off is not ctx:
         lat_alone_off, _ = d_latencies(False, ctx_off)
         lat_under_off, _ = d_latencies(True, ctx_off)
@@ -701,13 +720,13 @@ def main():
     ph_d, name_d = dom
     ms_d, n_d = kern[dom]
     avg_s = ms_d / n_d / 1e3
-    by, fl = kernel_units(spec, name_d, T[ph_d], rows[ph_d], touched[ph_d], esz)
+    by, fl = kernel_units(spec, name_d, T[ph_d], rows[ph_d], touched[ph_d], esz, osz)
     t_hbm = by / (HBM_PEAK_GBS * 1e9)
-    t_mfma = fl / (MFMA_BF16_PEAK_TFLOPS * 1e12) if bf16 else fl / (FP32_VECTOR_PEAK_TFLOPS * 1e12)
+    t_mfma = fl / (mma_peak * 1e12) if packed else fl / (FP32_VECTOR_PEAK_TFLOPS * 1e12)
     if fl and t_mfma >= t_hbm:
         achieved = fl / avg_s / 1e12
-        peak = MFMA_BF16_PEAK_TFLOPS if bf16 else FP32_VECTOR_PEAK_TFLOPS
-        roof = {"bound": "mfma" if bf16 else "alu", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s"}
+        peak = mma_peak if packed else FP32_VECTOR_PEAK_TFLOPS
+        roof = {"bound": "mfma" if packed else "alu", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s"}
     else:
         achieved = by / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
@@ -718,7 +737,7 @@ def main():
 
     kernels = {}
     for (ph, name), (ms, n) in sorted(kern.items()):
-        by_k, fl_k = kernel_units(spec, name, T[ph], rows[ph], touched[ph], esz)
+        by_k, fl_k = kernel_units(spec, name, T[ph], rows[ph], touched[ph], esz, osz)
         us = ms / n * 1e3
         kernels[f"{'P' if ph == 0 else 'D'}.{name}"] = {
             "mean_us": round(us, 2),
@@ -740,7 +759,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if bf16 else "f32",
+        "dtype": "fp8-mx" if fp8 else "bf16" if bf16 else "f32",
         "data": "synthetic",
         "config": {"workload": workload_name(spec), "E": spec.E, "E_loc": spec.E_loc, "top_k": spec.k, "H": spec.H,
                    "I": spec.I, "T_P": spec.T_P, "T_D": spec.T_D, "rows_P": rows[0], "rows_D": rows[1],

@@ -263,8 +263,9 @@ int layout(moe_ctx* ctx, Phase& p, hipStream_t stream) {
   const int T = p.T, k = c.top_k, E_loc = c.num_local_experts;
   chunking(T, k, E_loc, &p.chunk_tokens, &p.nchunks);
   if (c.dtype == MOE_DTYPE_FP8) {
-    p.regime = 1;
-    p.bm = ffn_mx_bm();
+    const long long avg = (long long)T * k / c.num_experts;
+    p.regime = avg >= 32 ? 0 : 1;
+    p.bm = ffn_mx_bm(p.regime);
   } else if (c.dtype == MOE_DTYPE_BF16) {
     // Rows per resident expert expected under even routing: T*k/E.  Small
     // batches stream weights (32-row tiles); large ones take 128-row tiles,
@@ -452,7 +453,7 @@ int moe_expert_ffn(moe_ctx_t* ctx, int phase, hipStream_t stream) {
     for (int gemm = 1; gemm <= 2; ++gemm) {
       st = timed(p, gemm == 1 ? MOE_KERNEL_GEMM1 : MOE_KERNEL_GEMM2, stream, [&] {
         if (c.dtype == MOE_DTYPE_FP8)
-          return launch_ffn_mx(gemm, p.b, mx_of(ctx, p),
+          return launch_ffn_mx(p.regime, gemm, p.b, mx_of(ctx, p),
                                MxWeights{ctx->w.w_gate_up, ctx->w.w_gate_up_scales, ctx->w.w_down, ctx->w.w_down_scales},
                                c.num_local_experts, c.hidden, c.inter, max_m_tiles, yield_of(ctx, phase), stream);
         if (c.dtype == MOE_DTYPE_BF16)

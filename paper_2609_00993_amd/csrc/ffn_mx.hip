@@ -16,11 +16,17 @@
 //    32 columns of a row (the two lanes holding a row's 32 columns exchange
 //    their maxima), GEMM2 writes float32 y.
 //
-// The GEMM here is the weight-streaming tile (32 rows x 128 columns, each
-// wave reading its operand rows straight into registers), which every batch
-// size uses.
+// Two tile shapes, as in the bf16 layer: the weight-streaming tile for small
+// batches (32 rows x 128 columns, each wave reading its operand rows straight
+// into registers) and, for large batches, 128 x 128 (gate + up) / 128 x 256
+// tiles staged through a three-slot LDS ring of 128-deep K slices (128 bytes
+// per row, the byte layout of the bf16 ring's 64-deep slices), with the
+// slices' scale bytes staged alongside.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
+#include "pipeline.h"
 #include "tiles.h"
 
 namespace moepd {
@@ -241,6 +247,267 @@ __device__ __forceinline__ void gemm_mx_skinny_tile(const GemmArgsMX& g, const T
   }
 }
 
+// ------------------------------------------------------------------ LDS ring (prefill)
+
+// One workgroup of 4 waves, a BM x BN output tile of one expert.  Per
+// 128-deep K slice, A (BM rows) and B (BR = NB x BN weight rows) travel HBM ->
+// LDS by 16-byte DMA into a ring of STAGES slots (swizzled like the bf16
+// ring), and each row's four scale bytes of the slice (one per 32 values) by
+// 4-byte DMA into the slot's scale area.  Every wave issues the same number
+// of DMA instructions per slice (padding with a repeat of an A-scale gather
+// into a spare area), so vmcnt counts retire exactly whole slices.  A slice
+// is two 64-deep MFMA steps; fragments of the next step are read from LDS
+// while the current step's MFMAs run.
+template <int BM, int BR, int WM, int WN, bool GATED, int STAGES>
+__device__ __forceinline__ void gemm_mx_ring_body(const GemmArgsMX& g) {
+  constexpr int NB = GATED ? 2 : 1;
+  constexpr int BN = BR / NB;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int FM = WTM / 32, FN = WTN / 32, FB = FN * NB;
+  constexpr int BK = 128;                           // K values (bytes) per slice
+  constexpr int CPR = 8;                            // 16-byte chunks per staged row
+  constexpr int RPI = 8;                            // rows per 16-byte DMA instruction
+  constexpr int A_INS = BM / RPI / 4, B_INS = BR / RPI / 4;
+  constexpr int SC_ALL = (BM + BR) / 64;            // 4-byte gathers of scale rows per slice
+  constexpr int SC_INS = (SC_ALL + 3) / 4;          // per wave, padded
+  constexpr int NPS = A_INS + B_INS + SC_INS;       // vector-memory ops per wave per slice
+  constexpr int A_CH = BM * CPR, B_CH = BR * CPR;
+  constexpr int SC_W = BM + BR + 64;                // scale words per slot (+ spare for padding)
+  constexpr int NRD = 2 * (FM + FB), NMF = FM * FB;
+  static_assert(WM * WN == 4, "four waves");
+  static_assert(A_INS * RPI * 4 == BM && B_INS * RPI * 4 == BR, "slices split into whole DMA instructions");
+  static_assert(BM % 64 == 0 && BR % 64 == 0, "scale gathers of 64 rows");
+  static_assert(FM * 32 == WTM && FN * 32 == WTN, "wave tile must be a multiple of 32x32");
+  static_assert(STAGES >= 2 && NPS * (STAGES - 1) < 64, "pipeline depth");
+  // each slot: A chunks, B chunks, then SC_W scale words (one array, so the
+  // compiler sees the DMA'd scale words and the ring as one object)
+  __shared__ u32x4 ring[STAGES][A_CH + B_CH + SC_W / 4];
+
+  const int lane = threadIdx.x & 63;
+  const int h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+  const int KT = g.K / BK;
+  const int KS = g.K / 32;  // scale bytes per row
+  const int lrow = lane / CPR, lphys = lane % CPR;
+
+  __amdgpu_buffer_rsrc_t a_rsrc;
+  uint32_t a_off[A_INS];
+  const uint8_t* b_src[B_INS];
+  const uint8_t* sc_src[SC_INS];  // this lane's scale word of slice 0 (rows clamped into range)
+  int sc_dst[SC_INS];             // its 64-word group in the slot's scale area
+  auto set_sources = [&](const TileCoord& tc) {
+    const int m0 = __builtin_amdgcn_readfirstlane(tc.m0);
+    const int rows = min(__builtin_amdgcn_readfirstlane(tc.m_end) - m0, BM);
+    a_rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(g.A + (size_t)m0 * g.K), (short)0, rows * g.K,
+                                               kBufferRsrcWord3);
+    const int e = __builtin_amdgcn_readfirstlane(tc.e);
+    const uint8_t* Be = g.B + (size_t)e * g.b_stride;
+    const uint8_t* Bse = g.Bs + (size_t)e * g.bs_stride;
+#pragma unroll
+    for (int i = 0; i < A_INS; ++i) {
+      const int r = (wave * A_INS + i) * RPI + lrow;
+      a_off[i] = (uint32_t)(r * g.K + (lphys ^ swz<64>(r)) * 16);
+    }
+    auto brow_of = [&](int r) {
+      if (GATED) return r < BN ? min(tc.n0 + r, g.N - 1) : g.up_row + min(tc.n0 + r - BN, g.N - 1);
+      return min(tc.n0 + r, g.N - 1);
+    };
+#pragma unroll
+    for (int i = 0; i < B_INS; ++i) {
+      const int r = (wave * B_INS + i) * RPI + lrow;
+      b_src[i] = Be + (size_t)brow_of(r) * g.K + (lphys ^ swz<64>(r)) * 16;
+    }
+    // Every gather is the same instruction (no branch in the K loop): A-scale
+    // rows past the expert's end are clamped to its last row (their outputs
+    // are never stored); padding gathers repeat rows 0..63 into the spare area.
+#pragma unroll
+    for (int i = 0; i < SC_INS; ++i) {
+      const int q = wave * SC_INS + i;
+      const int qq = q < SC_ALL ? q : 0;
+      const int r = qq * 64 + lane;
+      if (r < BM) sc_src[i] = g.As + (size_t)min(m0 + r, tc.m_end - 1) * KS;
+      else sc_src[i] = Bse + (size_t)brow_of(r - BM) * KS;
+      sc_dst[i] = __builtin_amdgcn_readfirstlane(q < SC_ALL ? q * 64 : BM + BR);
+    }
+  };
+  auto issue = [&](int kt, int slot) {
+#pragma unroll
+    for (int i = 0; i < A_INS; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, MOEPD_LPTR(&ring[slot][(wave * A_INS + i) * 64]), 16,
+                                               a_off[i] + (uint32_t)kt * BK, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < B_INS; ++i)
+      __builtin_amdgcn_global_load_lds(MOEPD_GPTR(b_src[i] + kt * BK),
+                                       MOEPD_LPTR(&ring[slot][A_CH + (wave * B_INS + i) * 64]), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < SC_INS; ++i)
+      __builtin_amdgcn_global_load_lds(MOEPD_GPTR(sc_src[i] + kt * 4),
+                                       MOEPD_LPTR(&ring[slot][A_CH + B_CH + sc_dst[i] / 4]), 4, 0, 0);
+  };
+  auto prologue = [&](const TileCoord& tc) {
+    set_sources(tc);
+#pragma unroll
+    for (int st = 0; st < STAGES; ++st)
+      if (st < KT) issue(st, st);
+  };
+
+  // step s of a slice: lane half h takes chunks 4s + h and 4s + 2 + h of its
+  // row (K [64s + 16h, +16) and [64s + 32 + 16h, +16)); its scale word holds
+  // the slice's four block scales, of which step s uses byte 2s + h.
+  v8i32 fa[2][FM], fb[2][FB];
+  uint32_t sa[FM], sb[FB];
+  auto read_frags = [&](int slot, int sub, v8i32 (&a)[FM], v8i32 (&b)[FB]) {
+    const u32x4* As = &ring[slot][0];
+    const u32x4* Bs = &ring[slot][A_CH];
+    const int c0 = 4 * sub + h, c1 = 4 * sub + 2 + h;
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+      const int r = wm * WTM + fm * 32 + (lane & 31);
+      a[fm] = join(As[r * CPR + (c0 ^ swz<64>(r))], As[r * CPR + (c1 ^ swz<64>(r))]);
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        const int r = nb * BN + wn * WTN + fn * 32 + (lane & 31);
+        b[nb * FN + fn] = join(Bs[r * CPR + (c0 ^ swz<64>(r))], Bs[r * CPR + (c1 ^ swz<64>(r))]);
+      }
+  };
+  auto read_scales = [&](int slot, uint32_t (&ra)[FM], uint32_t (&rb)[FB]) {
+    const u32x4* S = &ring[slot][A_CH + B_CH];
+    // 16-byte reads: LDS reads of 4 bytes right after the DMA issue made the
+    // compiler wait for every outstanding DMA (vmcnt(0)) in the K loop
+    auto word = [&](int i) {
+      const u32x4 v = S[i >> 2];
+      const int c = i & 3;
+      return c == 0 ? v[0] : c == 1 ? v[1] : c == 2 ? v[2] : v[3];
+    };
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) ra[fm] = word(wm * WTM + fm * 32 + (lane & 31)) >> (8 * h);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+        rb[nb * FN + fn] = word(BM + nb * BN + wn * WTN + fn * 32 + (lane & 31)) >> (8 * h);
+  };
+
+  f32x16_mx acc[FM][FB];
+  auto mfmas = [&](int sub, const v8i32 (&a)[FM], const v8i32 (&b)[FB]) {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int j = 0; j < FB; ++j)
+        acc[fm][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b[j], a[fm], acc[fm][j], 0, 0, 0,
+                                                                     (int)(sb[j] >> (16 * sub)), 0,
+                                                                     (int)(sa[fm] >> (16 * sub)));
+  };
+
+  const int L = block_tile(g);
+  if (L < 0) return;
+  yield_to_window(g.yield);
+  TileCoord tc;
+  tile_at(g, L, BM, BN, tc);
+  prologue(tc);
+
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FB; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  wait_slices_lgkm0<NPS, STAGES - 1>(min(STAGES - 1, KT - 1));
+  bare_barrier();
+  read_frags(0, 0, fa[0], fb[0]);
+  read_scales(0, sa, sb);
+
+  // One K slice (MODE as in the bf16 ring: 0 refills the slot, 1 has nothing
+  // left to issue, 2 is the last slice).
+  auto slice = [&](auto mode, int kt, int slot) {
+    constexpr int MODE = decltype(mode)::value;
+    // step 0: read step 1's fragments, multiply step 0
+    read_frags(slot, 1, fa[1], fb[1]);
+    mfmas(0, fa[0], fb[0]);
+    interleave<0, NMF, 0, NRD, 0>();
+    if constexpr (MODE < 2) {
+      if constexpr (MODE == 0) wait_vmcnt_lgkm0<NPS * (STAGES - 2)>();
+      else wait_slices_lgkm0<NPS, STAGES - 2>(min(STAGES - 2, KT - 2 - kt));
+      bare_barrier();
+      int ns = slot + 1;
+      if (ns == STAGES) ns = 0;
+      if constexpr (MODE == 0) issue(kt + STAGES, slot);
+      uint32_t na[FM], nb[FB];
+      read_frags(ns, 0, fa[0], fb[0]);
+      read_scales(ns, na, nb);
+      mfmas(1, fa[1], fb[1]);
+      interleave<0, NMF, MODE == 0 ? NPS : 0, NRD + FM + FB, 1>();
+#pragma unroll
+      for (int i = 0; i < FM; ++i) sa[i] = na[i];
+#pragma unroll
+      for (int j = 0; j < FB; ++j) sb[j] = nb[j];
+    } else {
+      mfmas(1, fa[1], fb[1]);
+    }
+  };
+  int kt = 0, slot = 0;
+  for (; kt < KT - STAGES; ++kt) {
+    slice(std::integral_constant<int, 0>{}, kt, slot);
+    if (++slot == STAGES) slot = 0;
+  }
+  for (; kt < KT - 1; ++kt) {
+    slice(std::integral_constant<int, 1>{}, kt, slot);
+    if (++slot == STAGES) slot = 0;
+  }
+  slice(std::integral_constant<int, 2>{}, kt, slot);
+
+  // epilogue (lane l: row l & 31 of each 32-row block, columns 8q + 4h + t)
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    const int row = tc.m0 + wm * WTM + fm * 32 + (lane & 31);
+    const bool live = row < tc.m_end;
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const int col0 = tc.n0 + wn * WTN + fn * 32;  // a 32-column block: all in range or all out
+      if (GATED) {
+        float v[16];
+        float amax = 0.f;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          v[q] = silu_mul_mx(acc[fm][fn][q], acc[fm][FN + fn][q]);
+          amax = fmaxf(amax, fabsf(v[q]));
+        }
+        amax = fmaxf(amax, __shfl_xor(amax, 32, kWave));
+        if (!live || col0 >= g.N) continue;
+        const int e = mx_exponent(amax);
+        const float inv = pow2_neg(e);
+        uint8_t* hrow = static_cast<uint8_t*>(g.C) + (size_t)row * g.N + col0 + 4 * h;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t w = e4m3_pair(v[4 * q] * inv, v[4 * q + 1] * inv) |
+                             (e4m3_pair(v[4 * q + 2] * inv, v[4 * q + 3] * inv) << 16);
+          *reinterpret_cast<uint32_t*>(hrow + 8 * q) = w;
+        }
+        if (h == 0) g.Cs[(size_t)row * (g.N / 32) + col0 / 32] = (uint8_t)(e + 127);
+      } else {
+        if (!live || col0 >= g.N) continue;
+        float* yrow = static_cast<float*>(g.C) + (size_t)row * g.N + col0 + 4 * h;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<f32x4_mx*>(yrow + 8 * q) =
+              f32x4_mx{acc[fm][fn][4 * q], acc[fm][fn][4 * q + 1], acc[fm][fn][4 * q + 2], acc[fm][fn][4 * q + 3]};
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void gemm1_mx_prefill(GemmArgsMX g) {
+  gemm_mx_ring_body<128, 256, 2, 2, true, 3>(g);
+}
+__global__ __launch_bounds__(256) void gemm2_mx_prefill(GemmArgsMX g) {
+  gemm_mx_ring_body<128, 256, 2, 2, false, 3>(g);
+}
+
 template <bool GATED>
 __global__ __launch_bounds__(256) void gemm_mx_skinny(GemmArgsMX g) {
   const int L = block_tile(g);
@@ -253,8 +520,8 @@ __global__ __launch_bounds__(256) void gemm_mx_skinny(GemmArgsMX g) {
 
 static inline int round8_mx(long long v) { return (int)((v + 7) / 8 * 8); }
 
-hipError_t launch_ffn_mx(int gemm, const PhaseBuffers& b, const MxBuffers& mx, const MxWeights& w, int e_loc, int H,
-                         int I, int max_m_tiles, YieldTo yield, hipStream_t s) {
+hipError_t launch_ffn_mx(int regime, int gemm, const PhaseBuffers& b, const MxBuffers& mx, const MxWeights& w,
+                         int e_loc, int H, int I, int max_m_tiles, YieldTo yield, hipStream_t s) {
   GemmArgsMX g{};
   g.offsets = b.offsets;
   g.tile_base = b.tile_base;
@@ -287,13 +554,20 @@ hipError_t launch_ffn_mx(int gemm, const PhaseBuffers& b, const MxBuffers& mx, c
     g.K = I;
     g.up_row = 0;
   }
-  g.n_tiles = (g.N + 127) / 128;
-  const dim3 grid(round8_mx((long long)max_m_tiles * g.n_tiles));
-  if (gemm == 1) gemm_mx_skinny<true><<<grid, 256, 0, s>>>(g);
-  else gemm_mx_skinny<false><<<grid, 256, 0, s>>>(g);
+  if (regime == 0) {
+    g.n_tiles = gemm == 1 ? (g.N + 127) / 128 : (g.N + 255) / 256;
+    const dim3 grid(round8_mx((long long)max_m_tiles * g.n_tiles));
+    if (gemm == 1) gemm1_mx_prefill<<<grid, 256, 0, s>>>(g);
+    else gemm2_mx_prefill<<<grid, 256, 0, s>>>(g);
+  } else {
+    g.n_tiles = (g.N + 127) / 128;
+    const dim3 grid(round8_mx((long long)max_m_tiles * g.n_tiles));
+    if (gemm == 1) gemm_mx_skinny<true><<<grid, 256, 0, s>>>(g);
+    else gemm_mx_skinny<false><<<grid, 256, 0, s>>>(g);
+  }
   return hipGetLastError();
 }
 
-int ffn_mx_bm() { return 32; }
+int ffn_mx_bm(int regime) { return regime == 0 ? 128 : 32; }
 
 }  // namespace moepd

@@ -126,9 +126,11 @@ struct MxWeights {
 // x (bf16 rows) -> MX FP8 codes and scales of every resident row.
 hipError_t launch_permute_mx(const void* x, int T, int k, int H, const int32_t* row_of_slot, uint8_t* codes,
                              uint8_t* scales, hipStream_t s);
-int ffn_mx_bm();
-hipError_t launch_ffn_mx(int gemm, const PhaseBuffers& b, const MxBuffers& mx, const MxWeights& w, int e_loc, int H,
-                         int I, int max_m_tiles, YieldTo yield, hipStream_t s);
+// regime 0: large batches (128-row LDS-ring tiles); 1: small batches
+// (32-row weight-streaming tiles).
+int ffn_mx_bm(int regime);
+hipError_t launch_ffn_mx(int regime, int gemm, const PhaseBuffers& b, const MxBuffers& mx, const MxWeights& w,
+                         int e_loc, int H, int I, int max_m_tiles, YieldTo yield, hipStream_t s);
 
 int ffn_f32_bm();
 hipError_t launch_ffn_f32(int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn, int e_loc, int H,

@@ -77,6 +77,7 @@ class GpuLayer:
         self.x = {ph: to_dev(inp.x_bits[ph] if packed else inp.x[ph]) for ph in (0, 1)}
         self.logits = {ph: to_dev(inp.logits[ph]) for ph in (0, 1)}
         self.out = {ph: torch.zeros((self.T[ph], spec.H), dtype=torch.float32, device="cuda") for ph in (0, 1)}
+        torch.cuda.synchronize()  # the fills run on torch's stream, which ours do not wait for
         dt = M.MOE_DTYPE_FP8 if self.fp8 else M.MOE_DTYPE_BF16 if self.bf16 else M.MOE_DTYPE_F32
         cfg = M.make_config(spec.E, spec.e0, spec.E_loc, spec.k, spec.H, spec.I, dt, max_tokens[0], max_tokens[1],
                             d_priority_us=d_priority_us)

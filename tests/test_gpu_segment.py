@@ -44,11 +44,12 @@ def setup():
     xs = [to_dev(p.x_bits[0]) for p in per]
     lg = [to_dev(p.logits[0]) for p in per]
     M = g.M
-    solo = []
+    # Buffers are filled on torch's current stream, which our streams do not
+    # wait for: synchronize before any of our work writes them.
+    solo = [torch.zeros((SPEC.T_P, SPEC.H), dtype=torch.float32, device="cuda") for _ in range(LAYERS)]
+    torch.cuda.synchronize()
     for l in range(LAYERS):
-        o = torch.zeros((SPEC.T_P, SPEC.H), dtype=torch.float32, device="cuda")
-        M.layer(g.ctx, 0, lg[l], SPEC.T_P, xs[l], o, g.streams[0])
-        solo.append(o)
+        M.layer(g.ctx, 0, lg[l], SPEC.T_P, xs[l], solo[l], g.streams[0])
     g.run(1)
     torch.cuda.synchronize()
     d_ref = g.out[1].clone()
@@ -82,6 +83,7 @@ def test_split_dispatch_matches_fused(setup):
     M.check(M.moe_dispatch_permute(ctx, 0, xs[0], s))
     M.check(M.moe_expert_ffn(ctx, 0, s))
     out = torch.zeros_like(solo[0])
+    torch.cuda.synchronize()
     M.check(M.moe_combine(ctx, 0, out, s))
     torch.cuda.synchronize()
     assert torch.equal(out, solo[0])
@@ -104,6 +106,8 @@ def test_segmented_epoch_matches_back_to_back(setup, K, d_enqueued):
     M, ctx = g.M, g.ctx
     print(f"[segment] K={K} d_enqueued={d_enqueued} layers={LAYERS}", flush=True)
     outs = [torch.full_like(solo[0], float("nan")) for _ in range(LAYERS)]
+    d_bufs = [torch.zeros_like(d_ref) for _ in range(LAYERS + 2)]
+    torch.cuda.synchronize()
     st, ts = M.moe_turnstile_create(K, 4096)
     M.check(st)
     d_outs = []
@@ -117,7 +121,7 @@ def test_segmented_epoch_matches_back_to_back(setup, K, d_enqueued):
                 if q.task == M.MOE_TS_DONE:
                     M.check(M.moe_turnstile_release(ts))
                     break
-                o = torch.zeros_like(d_ref)
+                o = d_bufs[len(d_outs)]
                 M.layer(ctx, 1, g.logits[1], SPEC.T_D, g.x[1], o, g.streams[1])
                 d_outs.append(o)
                 M.check(M.moe_turnstile_release(ts))
@@ -145,6 +149,7 @@ def test_ready_d_runs_before_p_touches_the_gpu(setup):
     g, xs, lg, solo, _ = setup
     M, ctx = g.M, g.ctx
     outs = [torch.zeros_like(solo[0]) for _ in range(LAYERS)]
+    torch.cuda.synchronize()
     st, ts = M.moe_turnstile_create(LAYERS, 256)
     M.check(st)
     try:

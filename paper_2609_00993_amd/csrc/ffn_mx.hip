@@ -356,6 +356,7 @@ __device__ __forceinline__ void gemm_mx_ring_body(const GemmArgsMX& g) {
   // row (K [64s + 16h, +16) and [64s + 32 + 16h, +16)); its scale word holds
   // the slice's four block scales, of which step s uses byte 2s + h.
   v8i32 fa[2][FM], fb[2][FB];
+  u32x4 sa_raw[FM], sb_raw[FB];
   uint32_t sa[FM], sb[FB];
   auto read_frags = [&](int slot, int sub, v8i32 (&a)[FM], v8i32 (&b)[FB]) {
     const u32x4* As = &ring[slot][0];
@@ -374,22 +375,23 @@ __device__ __forceinline__ void gemm_mx_ring_body(const GemmArgsMX& g) {
         b[nb * FN + fn] = join(Bs[r * CPR + (c0 ^ swz<64>(r))], Bs[r * CPR + (c1 ^ swz<64>(r))]);
       }
   };
-  auto read_scales = [&](int slot, uint32_t (&ra)[FM], uint32_t (&rb)[FB]) {
+  // Scale words are read as whole 16-byte groups (4-byte LDS reads right
+  // after the DMA issue made the compiler wait for every outstanding DMA,
+  // vmcnt(0), in the K loop); the lane's word is picked when the slice
+  // starts, so the reads have the previous step's MFMAs to land.
+  auto read_scales = [&](int slot, u32x4 (&ra)[FM], u32x4 (&rb)[FB]) {
     const u32x4* S = &ring[slot][A_CH + B_CH];
-    // 16-byte reads: LDS reads of 4 bytes right after the DMA issue made the
-    // compiler wait for every outstanding DMA (vmcnt(0)) in the K loop
-    auto word = [&](int i) {
-      const u32x4 v = S[i >> 2];
-      const int c = i & 3;
-      return c == 0 ? v[0] : c == 1 ? v[1] : c == 2 ? v[2] : v[3];
-    };
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) ra[fm] = word(wm * WTM + fm * 32 + (lane & 31)) >> (8 * h);
+    for (int fm = 0; fm < FM; ++fm) ra[fm] = S[(wm * WTM + fm * 32 + (lane & 31)) >> 2];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn)
-        rb[nb * FN + fn] = word(BM + nb * BN + wn * WTN + fn * 32 + (lane & 31)) >> (8 * h);
+      for (int fn = 0; fn < FN; ++fn) rb[nb * FN + fn] = S[(BM + nb * BN + wn * WTN + fn * 32 + (lane & 31)) >> 2];
+  };
+  auto pick = [&](const u32x4& v) {  // the lane's word (rows are multiples of 4 apart), shifted to block h
+    const int c = lane & 3;
+    const uint32_t w = c == 0 ? v[0] : c == 1 ? v[1] : c == 2 ? v[2] : v[3];
+    return w >> (8 * h);
   };
 
   f32x16_mx acc[FM][FB];
@@ -420,12 +422,16 @@ __device__ __forceinline__ void gemm_mx_ring_body(const GemmArgsMX& g) {
   wait_slices_lgkm0<NPS, STAGES - 1>(min(STAGES - 1, KT - 1));
   bare_barrier();
   read_frags(0, 0, fa[0], fb[0]);
-  read_scales(0, sa, sb);
+  read_scales(0, sa_raw, sb_raw);
 
   // One K slice (MODE as in the bf16 ring: 0 refills the slot, 1 has nothing
   // left to issue, 2 is the last slice).
   auto slice = [&](auto mode, int kt, int slot) {
     constexpr int MODE = decltype(mode)::value;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) sa[i] = pick(sa_raw[i]);
+#pragma unroll
+    for (int j = 0; j < FB; ++j) sb[j] = pick(sb_raw[j]);
     // step 0: read step 1's fragments, multiply step 0
     read_frags(slot, 1, fa[1], fb[1]);
     mfmas(0, fa[0], fb[0]);
@@ -437,15 +443,10 @@ __device__ __forceinline__ void gemm_mx_ring_body(const GemmArgsMX& g) {
       int ns = slot + 1;
       if (ns == STAGES) ns = 0;
       if constexpr (MODE == 0) issue(kt + STAGES, slot);
-      uint32_t na[FM], nb[FB];
       read_frags(ns, 0, fa[0], fb[0]);
-      read_scales(ns, na, nb);
+      read_scales(ns, sa_raw, sb_raw);
       mfmas(1, fa[1], fb[1]);
       interleave<0, NMF, MODE == 0 ? NPS : 0, NRD + FM + FB, 1>();
-#pragma unroll
-      for (int i = 0; i < FM; ++i) sa[i] = na[i];
-#pragma unroll
-      for (int j = 0; j < FB; ++j) sb[j] = nb[j];
     } else {
       mfmas(1, fa[1], fb[1]);
     }

@@ -86,8 +86,9 @@ bool valid_config(const moe_config_t* c) {
   return true;
 }
 
-// Chunking of the dispatch histogram for T tokens: about 256 slots per chunk,
-// and never more than kMaxCells (expert, chunk) cells.
+// Chunking of the dispatch histogram for T tokens: one chunk up to
+// kOneChunkSlots slots, else about 256 slots per chunk, and never more than
+// kMaxCells (expert, chunk) cells.
 void chunking(int T, int k, int e_loc, int* tc_out, int* nchunks_out) {
   int tc = dispatch_chunk_tokens(T, k, e_loc);
   int nc = T > 0 ? (T + tc - 1) / tc : 1;
@@ -280,10 +281,13 @@ int layout(moe_ctx* ctx, Phase& p, hipStream_t stream) {
     p.regime = 0;
     p.bm = ffn_f32_bm();
   }
-  int st = timed(p, MOE_KERNEL_COUNT, stream, [&] {
-    return launch_count(p.b.topk_idx, T, k, c.expert_begin, E_loc, p.chunk_tokens, p.nchunks, p.b, stream);
-  });
-  if (st) return st;
+  int st = MOE_OK;
+  if (p.nchunks > 1) {  // one chunk: the place kernel counts its slots itself
+    st = timed(p, MOE_KERNEL_COUNT, stream, [&] {
+      return launch_count(p.b.topk_idx, T, k, c.expert_begin, E_loc, p.chunk_tokens, p.nchunks, p.b, stream);
+    });
+    if (st) return st;
+  }
   return timed(p, MOE_KERNEL_PLACE, stream, [&] {
     return launch_place(p.b.topk_idx, T, k, c.expert_begin, E_loc, p.chunk_tokens, p.nchunks, p.bm, p.b, stream);
   });

@@ -10,7 +10,8 @@
 // with LDS integer atomics (order-free), and ranks come from wave ballots
 // taken in slot order, so the layout is bit-exact and reproducible.
 //
-// Tokens are cut into chunks of `chunk_tokens`.  The count kernel writes one
+// Tokens are cut into chunks of `chunk_tokens` (a small batch is one chunk,
+// which the place kernel counts itself).  The count kernel writes one
 // histogram cell per (expert, chunk).  The place kernel (the next launch, so
 // every cell is visible without device-scope fences) scans the cells in
 // expert-major order in LDS, which yields the first row of every (expert,
@@ -79,7 +80,18 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
 
   // exclusive scan of all (expert, chunk) cells, expert-major
   const int n = e_loc * nchunks;  // <= kMaxCells (host guarantees)
-  for (int i = tid; i < n; i += 256) cells[i] = b.chunk_counts[i];
+  if (nchunks == 1) {
+    // one chunk: count its slots here (LDS integer atomics, order-free)
+    for (int i = tid; i < n; i += 256) cells[i] = 0;
+    __syncthreads();
+    const long long ns = (long long)T * k;
+    for (long long s = tid; s < ns; s += 256) {
+      const int le = local_expert(topk_idx[s], e0, e_loc);
+      if (le >= 0) atomicAdd(&cells[le], 1);
+    }
+  } else {
+    for (int i = tid; i < n; i += 256) cells[i] = b.chunk_counts[i];
+  }
   __syncthreads();
   const int seg = (n + 255) / 256;
   const int lo = min(n, tid * seg), hi = min(n, lo + seg);

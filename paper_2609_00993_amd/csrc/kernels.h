@@ -52,8 +52,14 @@ constexpr int kMaxTopK = 16;
 constexpr int kMaxExperts = 1024;
 constexpr int kMaxLocalExperts = 256;
 
+// Batches of at most this many slots take one chunk: the place kernel then
+// counts them itself and the count kernel is not launched (small D batches
+// save a launch).
+constexpr int kOneChunkSlots = 2048;
+
 // Dispatch chunking: tokens per chunk for a batch of T tokens.
 inline int dispatch_chunk_tokens(int T, int k, int e_loc) {
+  if ((long long)T * k <= kOneChunkSlots) return T > 0 ? T : 1;
   int tc = (256 + k - 1) / k;
   int need = (int)(((long long)T * e_loc + kMaxCells - 1) / kMaxCells);
   if (need > tc) tc = need;
@@ -90,6 +96,8 @@ hipError_t launch_count(const int32_t* topk_idx, int T, int k, int e0, int e_loc
 // Scan of the histogram cells (block 0 publishes counts, offsets and the
 // m-tile prefix for m-tiles of bm rows) and stable rows for every slot:
 // row_of_slot and token_of_row.  Launched for every batch, T = 0 included.
+// With one chunk (nchunks == 1) the kernel counts the slots itself and the
+// count kernel is not launched.
 hipError_t launch_place(const int32_t* topk_idx, int T, int k, int e0, int e_loc, int chunk_tokens, int nchunks,
                         int bm, const PhaseBuffers& b, hipStream_t s);
 

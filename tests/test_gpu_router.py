@@ -19,8 +19,9 @@ import numpy as np
 import pytest
 
 import oracle
-from synth import BF16, F32, LayerSpec, f32_to_bf16_bits, bf16_bits_to_f32, make_config, make_layer
-from tests.gpu_util import GpuLayer, W_RTOL, assert_close_rms, read_dev, to_dev, tol_of
+from oracle import mx as OX
+from synth import BF16, F32, FP8, LayerSpec, f32_to_bf16_bits, bf16_bits_to_f32, make_config, make_layer
+from tests.gpu_util import GpuLayer, W_RTOL, assert_close_rms, read_dev, rms, to_dev, tol_of
 
 pytestmark = pytest.mark.gpu
 
@@ -44,6 +45,9 @@ SPECS = {
                                                   dtype=BF16, T_P=300, T_D=5), seed=17),
     "ragged-f32": lambda: make_layer(LayerSpec("ragged-f32", E=12, e0=3, E_loc=6, k=2, H=192, I=128, dtype=F32,
                                                T_P=77, T_D=0), seed=16),
+    # FP8 contexts gate on bf16 hidden states with a bf16 gate matrix
+    "fp8": lambda: make_layer(LayerSpec("fp8", E=40, e0=5, E_loc=16, k=3, H=256, I=384, dtype=FP8, T_P=700,
+                                        T_D=7), seed=18),
 }
 
 U = 2.0 ** -24
@@ -53,7 +57,7 @@ def router_inputs(inp, with_bias):
     """Gate matrix as [E, H] in the context dtype: device array and the values
     the oracle takes."""
     wt = np.ascontiguousarray(inp.wg.T)
-    if inp.spec.dtype == BF16:
+    if inp.spec.dtype in (BF16, FP8):
         bits = f32_to_bf16_bits(wt)
         vals = bf16_bits_to_f32(bits)
         dev = to_dev(bits)
@@ -126,9 +130,15 @@ def test_route_from_hidden(name, with_bias):
             M.check(M.moe_combine(g.ctx, ph, g.out[ph], s))
         for ph in (0, 1):
             lg = check_router(g, inp, ph, w_vals, bias)
-            ref = oracle.layer(lg, inp.x[ph], inp.w_gu, inp.w_dn, spec.k, spec.e0)
             torch.cuda.synchronize()
-            assert_close_rms(g.out[ph].cpu().numpy(), ref["out"], tol_of(spec), f"{name} ph{ph} out")
+            if spec.dtype == FP8:
+                ref = OX.layer_mx(lg, inp.x[ph], inp.w_gu_bits, inp.w_gu_scales, inp.w_dn_bits, inp.w_dn_scales,
+                                  spec.k, spec.e0)
+                d = rms(g.out[ph].cpu().numpy() - ref["out"]) / max(rms(ref["out"]), 1e-30)
+                assert d <= 2e-2, f"{name} ph{ph} out: RMS difference {d:.3e}"  # the FP8 layer's bar
+            else:
+                ref = oracle.layer(lg, inp.x[ph], inp.w_gu, inp.w_dn, spec.k, spec.e0)
+                assert_close_rms(g.out[ph].cpu().numpy(), ref["out"], tol_of(spec), f"{name} ph{ph} out")
         # a second call gives the same bits (fixed split order)
         first = {ph: read_dev(M.moe_phase_view(g.ctx, ph)[1].logits, (g.T[ph], spec.E), np.float32)
                  for ph in (0, 1)}

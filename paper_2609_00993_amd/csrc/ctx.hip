@@ -271,9 +271,9 @@ int layout(moe_ctx* ctx, Phase& p, hipStream_t stream) {
     p.bm = ffn_mx_bm(p.regime);
   } else if (c.dtype == MOE_DTYPE_BF16) {
     // Rows per resident expert expected under even routing: T*k/E.  Small
-    // batches stream weights (32-row tiles); large ones take 128-row tiles,
-    // and very large ones 256-row tiles, which move a third fewer bytes into
-    // LDS per flop.
+    // batches stream weights (32-row tiles); large ones take 160-row tiles,
+    // and very large ones 256-row tiles, which move fewer bytes into LDS per
+    // flop.
     const long long avg = (long long)T * k / c.num_experts;
     p.regime = avg >= 512 ? 2 : avg >= 32 ? 0 : 1;
     p.bm = ffn_bf16_bm(p.regime);

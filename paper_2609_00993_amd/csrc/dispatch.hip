@@ -73,7 +73,8 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
   int* cells = lds_dyn;
   int* base = cells + e_loc * nchunks;
   int* run = base + e_loc;
-  int(*wcnt)[kMaxLocalExperts + 1] = reinterpret_cast<int(*)[kMaxLocalExperts + 1]>(run + e_loc + 1);
+  const int ws = e_loc + 1;    // row stride of the per-wave counts
+  int* wcnt = run + e_loc + 1;  // [4][e_loc + 1]
   __shared__ int wave_tot[4];
   const int tid = threadIdx.x, w = tid >> 6;
   const int c = blockIdx.x;
@@ -129,7 +130,7 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
   }
   for (int i = tid; i <= e_loc; i += 256) {
     run[i] = 0;
-    wcnt[0][i] = wcnt[1][i] = wcnt[2][i] = wcnt[3][i] = 0;
+    wcnt[i] = wcnt[ws + i] = wcnt[2 * ws + i] = wcnt[3 * ws + i] = 0;
   }
   __syncthreads();
 
@@ -150,12 +151,12 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
       match &= on ? bal : ~bal;
     }
     const int rank = __popcll(match & lt);
-    if (rank == 0 && cat > 0) wcnt[w][cat] = __popcll(match);
+    if (rank == 0 && cat > 0) wcnt[w * ws + cat] = __popcll(match);
     __syncthreads();
     if (valid) {
       if (le >= 0) {
         int pre = run[cat];
-        for (int v = 0; v < w; ++v) pre += wcnt[v][cat];
+        for (int v = 0; v < w; ++v) pre += wcnt[v * ws + cat];
         const int row = base[le] + pre + rank;
         b.row_of_slot[s] = row;
         b.token_of_row[row] = (int)(s / k);
@@ -165,8 +166,8 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
     }
     __syncthreads();
     for (int i = tid; i <= e_loc; i += 256) {
-      run[i] += wcnt[0][i] + wcnt[1][i] + wcnt[2][i] + wcnt[3][i];
-      wcnt[0][i] = wcnt[1][i] = wcnt[2][i] = wcnt[3][i] = 0;
+      run[i] += wcnt[i] + wcnt[ws + i] + wcnt[2 * ws + i] + wcnt[3 * ws + i];
+      wcnt[i] = wcnt[ws + i] = wcnt[2 * ws + i] = wcnt[3 * ws + i] = 0;
     }
     __syncthreads();
   }
@@ -221,7 +222,7 @@ hipError_t launch_place(const int32_t* topk_idx, int T, int k, int e0, int e_loc
                         int bm, const PhaseBuffers& b, hipStream_t s) {
   int nbits = 0;
   while ((1 << nbits) <= e_loc) ++nbits;  // categories 0..e_loc
-  const size_t lds = sizeof(int) * ((size_t)e_loc * nchunks + e_loc + (e_loc + 1) + 4 * (kMaxLocalExperts + 1));
+  const size_t lds = sizeof(int) * ((size_t)e_loc * nchunks + e_loc + 5 * (size_t)(e_loc + 1));
   place_kernel<<<dim3(nchunks), dim3(256), lds, s>>>(topk_idx, T, k, e0, e_loc, chunk_tokens, nchunks, nbits, bm, b);
   return hipGetLastError();
 }

@@ -17,11 +17,16 @@
 // one expert that share a weight tile run side by side on one XCD's L2.
 //
 // Two tile shapes:
-//  * large batches (prefill): 256 threads, 128 x (128 gate + 128 up) or
-//    128 x 256 output tiles, 32x32x16 MFMAs.  Operands stream HBM -> LDS with
-//    global_load_lds_dwordx4 into a ring of three 64-deep K slices; fragments
-//    are double-buffered in registers and the LDS reads and DMA issues are
-//    interleaved with the MFMAs (see gemm_ring_body);
+//  * large batches (prefill): 256 threads, 160 x (128 gate + 128 up) or
+//    160 x 256 output tiles, 32x32x16 MFMAs, the four waves side by side
+//    along N.  Operands stream HBM -> LDS with global_load_lds_dwordx4 into a
+//    ring of three 64-deep K slices (156 KB); fragments are double-buffered
+//    in registers and the LDS reads and DMA issues are interleaved with the
+//    MFMAs (see gemm_ring_body).  160 rows, where 128 would be the plain
+//    choice, because an expert's rows are shared evenly among its m-tiles:
+//    with a few hundred rows per expert, ceil(rows / 160) saves the third,
+//    mostly empty m-tile that ceil(rows / 128) adds whenever an expert holds
+//    a little more than 256 rows, and every m-tile re-streams the weights;
 //  * small batches (decode, a few rows per expert): the layer is a weight
 //    stream, so each wave reads its weight rows straight into MFMA operand
 //    registers (no LDS round trip), one 32-row m-tile and 32 columns per wave,
@@ -412,8 +417,8 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
 }
 
 // Distinct entry points so that profiles name each GEMM of each regime.
-__global__ __launch_bounds__(256) void gemm1_swiglu_prefill(GemmArgs g) { gemm_ring_body<128, 256, 64, 2, 2, true, 3>(g); }
-__global__ __launch_bounds__(256) void gemm2_down_prefill(GemmArgs g) { gemm_ring_body<128, 256, 64, 2, 2, false, 3>(g); }
+__global__ __launch_bounds__(256) void gemm1_swiglu_prefill(GemmArgs g) { gemm_ring_body<160, 256, 64, 1, 4, true, 3>(g); }
+__global__ __launch_bounds__(256) void gemm2_down_prefill(GemmArgs g) { gemm_ring_body<160, 256, 64, 1, 4, false, 3>(g); }
 // The router GEMM: logits = x Wr^T over all T rows, 64 x 128 tiles, K split
 // so that small batches still spread over the GPU.
 __global__ __launch_bounds__(256) void router_gemm(GemmArgs g) { gemm_ring_body<64, 128, 64, 2, 2, false, 3, true>(g); }
@@ -426,7 +431,7 @@ __global__ __launch_bounds__(256) void gemm2_down_decode(GemmArgs g) { gemm_skin
 
 // ------------------------------------------------------------------ launch
 
-int ffn_bf16_bm(int regime) { return regime == 0 ? 128 : regime == 2 ? 256 : 32; }
+int ffn_bf16_bm(int regime) { return regime == 0 ? 160 : regime == 2 ? 256 : 32; }
 
 static inline int round8(long long v) { return (int)((v + 7) / 8 * 8); }
 
@@ -456,7 +461,7 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
   }
   if (regime == 0 || regime == 2) {
     g.n_tiles = gemm == 1 ? (g.N + 127) / 128 : (g.N + 255) / 256;
-    // 128-row tiles (a few m-tiles per expert): the m-tiles of one n-tile
+    // 160-row tiles (a few m-tiles per expert): the m-tiles of one n-tile
     // run together on one XCD and share its weights in that XCD's L2.
     // 256-row tiles (large experts, many m-tiles): tiles are dealt to the
     // XCDs round-robin, so the whole GPU works through one expert at a time
@@ -468,6 +473,7 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
     if (regime == 0) {
       if (gemm == 1) gemm1_swiglu_prefill<<<grid, 256, 0, s>>>(g);
       else gemm2_down_prefill<<<grid, 256, 0, s>>>(g);
+
     } else {
       if (gemm == 1) gemm1_swiglu_wide<<<grid, 256, 0, s>>>(g);
       else gemm2_down_wide<<<grid, 256, 0, s>>>(g);

@@ -36,6 +36,13 @@ __device__ __forceinline__ void dense_tile_at(const G& g, int L, int bm, int bn,
 // consecutive tiles (which one XCD runs side by side, see block_tile) share
 // an activation row block across n_group n-tiles and a weight n-tile across
 // the m-tiles running together.  n_group = n_tiles is plain m-major order.
+// With XCD-local tiles an expert's rows are shared evenly among its m-tiles
+// (tile_base counts ceil(rows / bm) of them, so none holds more than bm rows
+// and none is empty): the m-tiles that stream one weight panel on one XCD
+// then move at one pace and keep meeting in L2, where an uneven split (full
+// tiles and a short rest) lets them drift apart along K and fetch the panel
+// from HBM again.  Tiles dealt round-robin over the XCDs start at multiples
+// of bm (measured faster for the 256-row tiles, which run that way).
 template <class G>
 __device__ __forceinline__ void tile_at(const G& g, int L, int bm, int bn, TileCoord& tc) {
   int lo = 0, hi = g.e_loc - 1;
@@ -56,9 +63,11 @@ __device__ __forceinline__ void tile_at(const G& g, int L, int bm, int bn, TileC
   }
   r = local - blk * mt_e * b;
   const int mt = r / bw, nt = blk * b + (r - mt * bw);
+  const int beg = g.offsets[e], rows = g.offsets[e + 1] - beg;
+  const int per = g.xcd_local ? (rows + mt_e - 1) / mt_e : bm;
   tc.e = e;
-  tc.m0 = g.offsets[e] + mt * bm;
-  tc.m_end = g.offsets[e + 1];
+  tc.m0 = beg + mt * per;
+  tc.m_end = min(tc.m0 + per, beg + rows);
   tc.n0 = nt * bn;
   tc.split = 0;
 }

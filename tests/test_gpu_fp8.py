@@ -49,7 +49,10 @@ SPECS = {
     "mid-fp8": LayerSpec("mid-fp8", E=32, e0=0, E_loc=32, k=4, H=2048, I=1024, dtype=FP8, T_P=2048, T_D=64),
     "k1-fp8": LayerSpec("k1-fp8", E=16, e0=0, E_loc=16, k=1, H=128, I=128, dtype=FP8, T_P=900, T_D=2),
     "empty-d-fp8": LayerSpec("empty-d-fp8", E=12, e0=3, E_loc=6, k=2, H=384, I=256, dtype=FP8, T_P=77, T_D=0),
+    # skewed routing: experts of a few to ~850 rows, several m-tiles each
+    "split-fp8": LayerSpec("split-fp8", E=16, e0=0, E_loc=16, k=2, H=256, I=384, dtype=FP8, T_P=2000, T_D=6),
 }
+BIAS = {"split-fp8": np.linspace(1.2, -1.2, 16).astype(np.float32)}
 
 
 def h_bound(h64, scales_gpu, mag):
@@ -128,7 +131,7 @@ def check_phase(g, inp, ph):
 def test_fp8_layer_parity(name):
     spec = SPECS[name]
     print(f"[fp8] {spec}", flush=True)
-    inp = make_layer(spec, seed=41)
+    inp = make_layer(spec, seed=41, bias=BIAS.get(name))
     g = GpuLayer(inp)
     try:
         for ph in (0, 1):

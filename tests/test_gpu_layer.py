@@ -63,6 +63,11 @@ SPECS = {
     # a pool above 256 experts (8 logits per lane), 64 resident, top-8
     "wide-pool-bf16": lambda: make_layer(LayerSpec("wide-bf16", E=300, e0=100, E_loc=64, k=8, H=128, I=192,
                                                    dtype=BF16, T_P=700, T_D=5), seed=15),
+    # skewed routing on the large-batch tiles: experts of 7 to 841 rows, so
+    # one to six m-tiles each, with rows that do not divide evenly among them
+    "split-bf16": lambda: make_layer(LayerSpec("split-bf16", E=16, e0=0, E_loc=16, k=2, H=256, I=320, dtype=BF16,
+                                               T_P=2000, T_D=6), seed=19,
+                                     bias=np.linspace(1.2, -1.2, 16).astype(np.float32)),
     "ragged-f32": lambda: make_layer(LayerSpec("ragged-f32", E=12, e0=3, E_loc=6, k=2, H=192, I=128, dtype=F32,
                                                T_P=77, T_D=0), seed=16),
 }

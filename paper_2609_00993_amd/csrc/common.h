@@ -30,16 +30,34 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
   return l == 0 ? 0ull : (~0ull >> (64 - l));
 }
 
-// Wave-wide maximum of a 64-bit key, all lanes receive the result.
+// One step of a wave maximum over DPP: each lane in the rows ROW_MASK
+// enables takes the larger of its key and the key DPP control CTRL names;
+// the other lanes keep their own.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint64_t dpp_max_step(uint64_t v) {
+  const uint32_t lo = uint32_t(v), hi = uint32_t(v >> 32);
+  const uint32_t olo = __builtin_amdgcn_update_dpp(lo, lo, CTRL, ROW_MASK, 0xF, false);
+  const uint32_t ohi = __builtin_amdgcn_update_dpp(hi, hi, CTRL, ROW_MASK, 0xF, false);
+  const uint64_t o = (uint64_t(ohi) << 32) | olo;
+  return o > v ? o : v;
+}
+
+// Wave-wide maximum of a 64-bit key, returned to all lanes.  Register moves
+// across lanes (DPP) rather than LDS-routed shuffles, so the k selections
+// of the top-k kernel are a short dependent chain: swaps within quads, then
+// rotations by 4 and 8 lanes give every lane its 16-lane row's maximum; two
+// row broadcasts (lane 15 of rows 0 and 2 into rows 1 and 3, then lane 31
+// into rows 2 and 3) leave the wave's maximum on lane 63, which is read out.
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    uint32_t lo = __shfl_xor(uint32_t(v), off, kWave);
-    uint32_t hi = __shfl_xor(uint32_t(v >> 32), off, kWave);
-    uint64_t o = (uint64_t(hi) << 32) | lo;
-    v = o > v ? o : v;
-  }
-  return v;
+  v = dpp_max_step<0xB1, 0xF>(v);   // quad_perm [1,0,3,2]
+  v = dpp_max_step<0x4E, 0xF>(v);   // quad_perm [2,3,0,1]
+  v = dpp_max_step<0x124, 0xF>(v);  // row_ror:4
+  v = dpp_max_step<0x128, 0xF>(v);  // row_ror:8
+  v = dpp_max_step<0x142, 0xA>(v);  // row_bcast:15
+  v = dpp_max_step<0x143, 0xC>(v);  // row_bcast:31
+  const uint32_t lo = __builtin_amdgcn_readlane(uint32_t(v), 63);
+  const uint32_t hi = __builtin_amdgcn_readlane(uint32_t(v >> 32), 63);
+  return (uint64_t(hi) << 32) | lo;
 }
 
 // Inclusive wave scan of int32.

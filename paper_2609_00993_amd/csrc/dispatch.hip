@@ -45,6 +45,23 @@ __device__ __forceinline__ int block_exclusive_scan_256(int v, int* wave_tot, in
   return base + inc - v;
 }
 
+// Slot (or cell) loads each thread keeps in flight: the layout kernels are
+// latency-bound, so a loop that loads one value and then waits on it would
+// pay a full memory round trip per 256 slots.
+constexpr int kLoadBatch = 8;
+static_assert(kOneChunkSlots <= kLoadBatch * 256, "a one-chunk batch is loaded in one go");
+
+// Category of slot s of [0, s1): its local expert + 1, or 0 (dropped or past
+// the end), for the kLoadBatch slots sb + 256 j + threadIdx.x.
+__device__ __forceinline__ void load_cats(const int32_t* __restrict__ topk_idx, long long sb, long long s1, int e0,
+                                          int e_loc, int (&cat)[kLoadBatch]) {
+#pragma unroll
+  for (int j = 0; j < kLoadBatch; ++j) {
+    const long long s = sb + (long long)j * 256 + threadIdx.x;
+    cat[j] = s < s1 ? local_expert(topk_idx[s], e0, e_loc) + 1 : 0;
+  }
+}
+
 __global__ __launch_bounds__(256) void count_kernel(const int32_t* __restrict__ topk_idx, int T, int k, int e0,
                                                     int e_loc, int chunk_tokens, int nchunks,
                                                     int32_t* __restrict__ cells) {
@@ -55,9 +72,12 @@ __global__ __launch_bounds__(256) void count_kernel(const int32_t* __restrict__ 
   __syncthreads();
   const long long s0 = (long long)c * chunk_tokens * k;
   const long long s1 = min((long long)T, (long long)(c + 1) * chunk_tokens) * k;
-  for (long long s = s0 + tid; s < s1; s += 256) {
-    const int le = local_expert(topk_idx[s], e0, e_loc);
-    if (le >= 0) atomicAdd(&hist[le], 1);
+  for (long long sb = s0; sb < s1; sb += kLoadBatch * 256) {
+    int cat[kLoadBatch];
+    load_cats(topk_idx, sb, s1, e0, e_loc, cat);
+#pragma unroll
+    for (int j = 0; j < kLoadBatch; ++j)
+      if (cat[j] > 0) atomicAdd(&hist[cat[j] - 1], 1);
   }
   __syncthreads();
   for (int i = tid; i < e_loc; i += 256) cells[i * nchunks + c] = hist[i];
@@ -78,6 +98,13 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
   __shared__ int wave_tot[4];
   const int tid = threadIdx.x, w = tid >> 6;
   const int c = blockIdx.x;
+  const long long s0 = (long long)c * chunk_tokens * k;
+  const long long s1 = min((long long)T, (long long)(c + 1) * chunk_tokens) * k;
+
+  // categories of this chunk's first kLoadBatch * 256 slots (all of them for
+  // a one-chunk batch), loaded once for the count and the ranks
+  int cat0[kLoadBatch];
+  load_cats(topk_idx, s0, s1, e0, e_loc, cat0);
 
   // exclusive scan of all (expert, chunk) cells, expert-major
   const int n = e_loc * nchunks;  // <= kMaxCells (host guarantees)
@@ -85,13 +112,31 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
     // one chunk: count its slots here (LDS integer atomics, order-free)
     for (int i = tid; i < n; i += 256) cells[i] = 0;
     __syncthreads();
-    const long long ns = (long long)T * k;
-    for (long long s = tid; s < ns; s += 256) {
-      const int le = local_expert(topk_idx[s], e0, e_loc);
-      if (le >= 0) atomicAdd(&cells[le], 1);
+#pragma unroll
+    for (int j = 0; j < kLoadBatch; ++j)
+      if (cat0[j] > 0) atomicAdd(&cells[cat0[j] - 1], 1);
+    for (long long sb = s0 + kLoadBatch * 256; sb < s1; sb += kLoadBatch * 256) {
+      int cat[kLoadBatch];
+      load_cats(topk_idx, sb, s1, e0, e_loc, cat);
+#pragma unroll
+      for (int j = 0; j < kLoadBatch; ++j)
+        if (cat[j] > 0) atomicAdd(&cells[cat[j] - 1], 1);
     }
   } else {
-    for (int i = tid; i < n; i += 256) cells[i] = b.chunk_counts[i];
+    // every cell in one round of loads (the count kernel's blocks wrote them
+    // through other XCDs' caches, so each load is a trip past this L2)
+    constexpr int kCellLoads = kMaxCells / 256;
+    int v[kCellLoads];
+#pragma unroll
+    for (int j = 0; j < kCellLoads; ++j) {
+      const int i = j * 256 + tid;
+      v[j] = i < n ? b.chunk_counts[i] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kCellLoads; ++j) {
+      const int i = j * 256 + tid;
+      if (i < n) cells[i] = v[j];
+    }
   }
   __syncthreads();
   const int seg = (n + 255) / 256;
@@ -107,25 +152,25 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
     acc += v;
   }
   __syncthreads();
-  for (int e = tid; e < e_loc; e += 256) base[e] = cells[e * nchunks + c];
+  // e_loc <= kMaxLocalExperts = 256: thread e owns expert e below
+  if (tid < e_loc) base[tid] = cells[tid * nchunks + c];
   if (c == 0) {
-    // publish the dispatch shape: counts, offsets, m-tile prefix
-    for (int e = tid; e < e_loc; e += 256) {
-      const int off = cells[e * nchunks];
-      const int nxt = (e + 1 < e_loc) ? cells[(e + 1) * nchunks] : total;
-      b.offsets[e] = off;
-      b.counts[e] = nxt - off;
-      run[e] = (nxt - off + bm - 1) / bm;
+    // publish the dispatch shape: counts, offsets, and the m-tile prefix
+    // (a block scan of the per-expert m-tile counts)
+    int mt = 0;
+    if (tid < e_loc) {
+      const int off = cells[tid * nchunks];
+      const int nxt = (tid + 1 < e_loc) ? cells[(tid + 1) * nchunks] : total;
+      b.offsets[tid] = off;
+      b.counts[tid] = nxt - off;
+      mt = (nxt - off + bm - 1) / bm;
     }
-    __syncthreads();
+    int mt_total;
+    const int tb = block_exclusive_scan_256(mt, wave_tot, &mt_total);
+    if (tid < e_loc) b.tile_base[tid] = tb;
     if (tid == 0) {
       b.offsets[e_loc] = total;
-      int t_acc = 0;
-      for (int e = 0; e < e_loc; ++e) {
-        b.tile_base[e] = t_acc;
-        t_acc += run[e];
-      }
-      b.tile_base[e_loc] = t_acc;
+      b.tile_base[e_loc] = mt_total;
     }
   }
   for (int i = tid; i <= e_loc; i += 256) {
@@ -135,41 +180,51 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
   __syncthreads();
 
   // stable ranks of this chunk's slots, 256 slots per round, in slot order
-  const long long s0 = (long long)c * chunk_tokens * k;
-  const long long s1 = min((long long)T, (long long)(c + 1) * chunk_tokens) * k;
   const uint64_t lt = lanemask_lt();
-  for (long long sb = s0; sb < s1; sb += 256) {
-    const long long s = sb + tid;
-    const bool valid = s < s1;
-    const int le = valid ? local_expert(topk_idx[s], e0, e_loc) : -1;
-    const int cat = le + 1;  // 0 = dropped or past the chunk
-    // lanes of this wave with the same category, via one ballot per bit
-    uint64_t match = ~0ull;
-    for (int bit = 0; bit < nbits; ++bit) {
-      const bool on = (cat >> bit) & 1;
-      const uint64_t bal = __ballot(on);
-      match &= on ? bal : ~bal;
+  for (long long sb0 = s0; sb0 < s1; sb0 += kLoadBatch * 256) {
+    int cat_r[kLoadBatch];
+    if (sb0 == s0) {
+#pragma unroll
+      for (int j = 0; j < kLoadBatch; ++j) cat_r[j] = cat0[j];
+    } else {
+      load_cats(topk_idx, sb0, s1, e0, e_loc, cat_r);
     }
-    const int rank = __popcll(match & lt);
-    if (rank == 0 && cat > 0) wcnt[w * ws + cat] = __popcll(match);
-    __syncthreads();
-    if (valid) {
-      if (le >= 0) {
-        int pre = run[cat];
-        for (int v = 0; v < w; ++v) pre += wcnt[v * ws + cat];
-        const int row = base[le] + pre + rank;
-        b.row_of_slot[s] = row;
-        b.token_of_row[row] = (int)(s / k);
-      } else {
-        b.row_of_slot[s] = -1;
+#pragma unroll
+    for (int j = 0; j < kLoadBatch; ++j) {
+      const long long sb = sb0 + (long long)j * 256;
+      if (sb >= s1) break;  // block-uniform
+      const long long s = sb + tid;
+      const bool valid = s < s1;
+      const int cat = cat_r[j];  // 0 = dropped or past the chunk
+      const int le = cat - 1;
+      // lanes of this wave with the same category, via one ballot per bit
+      uint64_t match = ~0ull;
+      for (int bit = 0; bit < nbits; ++bit) {
+        const bool on = (cat >> bit) & 1;
+        const uint64_t bal = __ballot(on);
+        match &= on ? bal : ~bal;
       }
+      const int rank = __popcll(match & lt);
+      if (rank == 0 && cat > 0) wcnt[w * ws + cat] = __popcll(match);
+      __syncthreads();
+      if (valid) {
+        if (le >= 0) {
+          int pre = run[cat];
+          for (int v = 0; v < w; ++v) pre += wcnt[v * ws + cat];
+          const int row = base[le] + pre + rank;
+          b.row_of_slot[s] = row;
+          b.token_of_row[row] = (int)(s / k);
+        } else {
+          b.row_of_slot[s] = -1;
+        }
+      }
+      __syncthreads();
+      for (int i = tid; i <= e_loc; i += 256) {
+        run[i] += wcnt[i] + wcnt[ws + i] + wcnt[2 * ws + i] + wcnt[3 * ws + i];
+        wcnt[i] = wcnt[ws + i] = wcnt[2 * ws + i] = wcnt[3 * ws + i] = 0;
+      }
+      __syncthreads();
     }
-    __syncthreads();
-    for (int i = tid; i <= e_loc; i += 256) {
-      run[i] += wcnt[i] + wcnt[ws + i] + wcnt[2 * ws + i] + wcnt[3 * ws + i];
-      wcnt[i] = wcnt[ws + i] = wcnt[2 * ws + i] = wcnt[3 * ws + i] = 0;
-    }
-    __syncthreads();
   }
 }
 

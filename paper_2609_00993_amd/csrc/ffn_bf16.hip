@@ -29,8 +29,9 @@
 //    a little more than 256 rows, and every m-tile re-streams the weights;
 //  * small batches (decode, a few rows per expert): the layer is a weight
 //    stream, so each wave reads its weight rows straight into MFMA operand
-//    registers (no LDS round trip), one 32-row m-tile and 32 columns per wave,
-//    with the next two 64-deep K blocks in flight while one is multiplied.
+//    registers (no LDS round trip), one 32-row m-tile and 32 columns per
+//    single-wave workgroup, with the next two 64-deep K blocks in flight
+//    while one is multiplied.
 #include <type_traits>
 
 #include "common.h"
@@ -86,8 +87,15 @@ __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 
 
 // ------------------------------------------------------------------ skinny (decode)
 
+// Waves (32 output columns each) per decode workgroup.  One: every wave
+// loads its own operands anyway, and with single-wave workgroups the tiles
+// spread evenly over the CUs whatever their count (four-wave workgroups at
+// 1.5 tiles per CU left half the CUs with two, which then set the pace).
+constexpr int kDecodeWaves = 1;
+
 template <bool GATED, bool ROT>
 __device__ __forceinline__ void gemm_skinny_tile(const GemmArgs& g, const TileCoord& tc) {
+  constexpr int BN = 32 * kDecodeWaves;
   constexpr int NB = GATED ? 2 : 1;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 31, kg = lane >> 5;
@@ -109,7 +117,7 @@ __device__ __forceinline__ void gemm_skinny_tile(const GemmArgs& g, const TileCo
     for (int q = 0; q < 16; ++q) acc[j][q] = 0.f;
 
   const int KB = g.K / 64;
-  const int krot = ROT ? k_rotation(tc, g.n_tiles, 128, KB) : 0;
+  const int krot = ROT ? k_rotation(tc, g.n_tiles, BN, KB) : 0;
   constexpr int PF = 2;  // 64-deep K blocks in flight per wave (a static register ring)
   u32x4 ra[PF][4], rb[PF][NB][4];
   auto load = [&](int kb, u32x4 (&a)[4], u32x4 (&b)[NB][4]) {
@@ -158,7 +166,7 @@ __device__ __forceinline__ void gemm_skinny_tile(const GemmArgs& g, const TileCo
 
 template <bool GATED, bool ROT>
 __device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
-  constexpr int BM = 32, BN = 128;
+  constexpr int BM = 32, BN = 32 * kDecodeWaves;
   const int L = block_tile(g);
   if (L < 0) return;
   yield_to_window(g.yield);
@@ -425,9 +433,9 @@ __global__ __launch_bounds__(256) void router_gemm(GemmArgs g) { gemm_ring_body<
 __global__ __launch_bounds__(256) void gemm1_swiglu_wide(GemmArgs g) { gemm_ring_body<256, 256, 32, 2, 2, true, 4>(g); }
 __global__ __launch_bounds__(256) void gemm2_down_wide(GemmArgs g) { gemm_ring_body<256, 256, 32, 2, 2, false, 4>(g); }
 template <bool ROT>
-__global__ __launch_bounds__(256) void gemm1_swiglu_decode(GemmArgs g) { gemm_skinny<true, ROT>(g); }
+__global__ __launch_bounds__(64 * kDecodeWaves) void gemm1_swiglu_decode(GemmArgs g) { gemm_skinny<true, ROT>(g); }
 template <bool ROT>
-__global__ __launch_bounds__(256) void gemm2_down_decode(GemmArgs g) { gemm_skinny<false, ROT>(g); }
+__global__ __launch_bounds__(64 * kDecodeWaves) void gemm2_down_decode(GemmArgs g) { gemm_skinny<false, ROT>(g); }
 
 // ------------------------------------------------------------------ launch
 
@@ -479,17 +487,18 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
       else gemm2_down_wide<<<grid, 256, 0, s>>>(g);
     }
   } else {
-    g.n_tiles = (g.N + 127) / 128;
+    constexpr int bn = 32 * kDecodeWaves, threads = 64 * kDecodeWaves;
+    g.n_tiles = (g.N + bn - 1) / bn;
     g.n_group = 1;
     g.xcd_local = 1;
     const dim3 grid(round8((long long)max_m_tiles * g.n_tiles));
     const bool rot = g.K % 2048 == 0;
     if (gemm == 1) {
-      if (rot) gemm1_swiglu_decode<true><<<grid, 256, 0, s>>>(g);
-      else gemm1_swiglu_decode<false><<<grid, 256, 0, s>>>(g);
+      if (rot) gemm1_swiglu_decode<true><<<grid, threads, 0, s>>>(g);
+      else gemm1_swiglu_decode<false><<<grid, threads, 0, s>>>(g);
     } else {
-      if (rot) gemm2_down_decode<true><<<grid, 256, 0, s>>>(g);
-      else gemm2_down_decode<false><<<grid, 256, 0, s>>>(g);
+      if (rot) gemm2_down_decode<true><<<grid, threads, 0, s>>>(g);
+      else gemm2_down_decode<false><<<grid, threads, 0, s>>>(g);
     }
   }
   return hipGetLastError();

@@ -509,13 +509,18 @@ __global__ __launch_bounds__(256) void gemm2_mx_prefill(GemmArgsMX g) {
   gemm_mx_ring_body<128, 256, 2, 2, false, 3>(g);
 }
 
+// Small batches: one wave (32 output columns) per workgroup, so that the
+// tiles spread evenly over the CUs whatever their count (with four-wave
+// workgroups, 1.5 tiles per CU left half the CUs with two).
+constexpr int kMxDecodeWaves = 1;
+
 template <bool GATED>
-__global__ __launch_bounds__(256) void gemm_mx_skinny(GemmArgsMX g) {
+__global__ __launch_bounds__(64 * kMxDecodeWaves) void gemm_mx_skinny(GemmArgsMX g) {
   const int L = block_tile(g);
   if (L < 0) return;
   yield_to_window(g.yield);
   TileCoord tc;
-  tile_at(g, L, 32, 128, tc);
+  tile_at(g, L, 32, 32 * kMxDecodeWaves, tc);
   gemm_mx_skinny_tile<GATED>(g, tc);
 }
 
@@ -561,10 +566,10 @@ hipError_t launch_ffn_mx(int regime, int gemm, const PhaseBuffers& b, const MxBu
     if (gemm == 1) gemm1_mx_prefill<<<grid, 256, 0, s>>>(g);
     else gemm2_mx_prefill<<<grid, 256, 0, s>>>(g);
   } else {
-    g.n_tiles = (g.N + 127) / 128;
+    g.n_tiles = (g.N + 32 * kMxDecodeWaves - 1) / (32 * kMxDecodeWaves);
     const dim3 grid(round8_mx((long long)max_m_tiles * g.n_tiles));
-    if (gemm == 1) gemm_mx_skinny<true><<<grid, 256, 0, s>>>(g);
-    else gemm_mx_skinny<false><<<grid, 256, 0, s>>>(g);
+    if (gemm == 1) gemm_mx_skinny<true><<<grid, 64 * kMxDecodeWaves, 0, s>>>(g);
+    else gemm_mx_skinny<false><<<grid, 64 * kMxDecodeWaves, 0, s>>>(g);
   }
   return hipGetLastError();
 }

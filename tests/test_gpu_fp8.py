@@ -51,6 +51,9 @@ SPECS = {
     "empty-d-fp8": LayerSpec("empty-d-fp8", E=12, e0=3, E_loc=6, k=2, H=384, I=256, dtype=FP8, T_P=77, T_D=0),
     # skewed routing: experts of a few to ~850 rows, several m-tiles each
     "split-fp8": LayerSpec("split-fp8", E=16, e0=0, E_loc=16, k=2, H=256, I=384, dtype=FP8, T_P=2000, T_D=6),
+    # the limits: 1024 experts, 256 resident, top-16
+    "limits-fp8": LayerSpec("limits-fp8", E=1024, e0=512, E_loc=256, k=16, H=128, I=128, dtype=FP8, T_P=4096,
+                            T_D=128),
 }
 BIAS = {"split-fp8": np.linspace(1.2, -1.2, 16).astype(np.float32)}
 

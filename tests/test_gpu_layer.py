@@ -68,6 +68,20 @@ SPECS = {
     "split-bf16": lambda: make_layer(LayerSpec("split-bf16", E=16, e0=0, E_loc=16, k=2, H=256, I=320, dtype=BF16,
                                                T_P=2000, T_D=6), seed=19,
                                      bias=np.linspace(1.2, -1.2, 16).astype(np.float32)),
+    # the limits: 1024 experts, 256 resident, top-16; P's layout at the
+    # 8192-cell bound (32 chunks x 256 experts), D's at the one-chunk bound
+    # (2048 slots)
+    "limits-bf16": lambda: make_layer(LayerSpec("limits-bf16", E=1024, e0=512, E_loc=256, k=16, H=128, I=128,
+                                                dtype=BF16, T_P=4096, T_D=128), seed=24),
+    # the longest rows: H = 16384 (GEMM1's K), then I = 16384 (GEMM2's K).
+    # All experts resident and I = 128 for the first: rounding h to bf16
+    # (GEMM2's operand; the oracle keeps it in float64) alone moves single
+    # outputs by up to 2.8 % of the output RMS with I = 64 and three of four
+    # experts elsewhere (zero rows dilute the RMS), by 1.3 % here
+    "max-h-bf16": lambda: make_layer(LayerSpec("max-h-bf16", E=4, e0=0, E_loc=4, k=1, H=16384, I=128, dtype=BF16,
+                                               T_P=300, T_D=5), seed=25),
+    "max-i-bf16": lambda: make_layer(LayerSpec("max-i-bf16", E=4, e0=1, E_loc=1, k=1, H=64, I=16384, dtype=BF16,
+                                               T_P=300, T_D=5), seed=26),
     "ragged-f32": lambda: make_layer(LayerSpec("ragged-f32", E=12, e0=3, E_loc=6, k=2, H=192, I=128, dtype=F32,
                                                T_P=77, T_D=0), seed=16),
 }

@@ -144,11 +144,12 @@ typedef struct moe_config {
   int32_t flags;             /* must be 0 */
   /* D-first admission, 0..1000 (0 = off).  Section 3.1: ready D work is
    * admitted before P, and a long P execution is cut into segments so that D
-   * advances between them (Section 4.2).  On one GPU a P segment is one tile
-   * of its grouped GEMMs: while a D layer is in flight (from the start of its
-   * moe_route kernel to the start of its moe_combine kernel), a P grouped-GEMM
-   * workgroup about to start a tile waits for the D layer, for at most about
-   * this many microseconds.  A scheduling hint only: results are unchanged. */
+   * advances between them (Section 4.2).  On one GPU a P segment is a run of
+   * K slices of one grouped-GEMM tile: while a D layer is in flight (from the
+   * start of its moe_route kernel to the start of its moe_combine kernel), a P
+   * grouped-GEMM workgroup about to start a tile, or at every fourth K slice
+   * of a running tile, waits for the D layer, for at most about this many
+   * microseconds each time.  A scheduling hint only: results are unchanged. */
   int32_t d_priority_us;
 } moe_config_t;
 

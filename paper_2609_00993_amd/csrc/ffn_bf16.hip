@@ -202,6 +202,22 @@ __device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
 // index, so the SwiGLU is applied in registers).  The K loop is branch-free:
 // rows past the expert's end are clamped to its last row and discarded at
 // the store, which keeps the MFMA and LDS-read schedule intact.
+// Slices between the in-tile checks of the D window (a power of two).
+constexpr int kPauseEvery = 4;
+
+// The D window word, read device-coherently by a load the compiler does not
+// track.  A tracked load read a check later made the compiler wait for every
+// outstanding operation (it cannot follow the count through the loop),
+// draining the DMA ring.  Untracked, it is one extra operation after the
+// slice's DMA: the ring's counted waits then wait for one more (a little
+// early, never late), and two slice waits later the load has completed;
+// its value is read kPauseEvery slices later.  It only steers a pause.
+__device__ __forceinline__ int load_untracked(const int32_t* word) {
+  int v;
+  asm volatile("global_load_dword %0, %1, off sc1" : "=v"(v) : "v"(word) : "memory");
+  return v;
+}
+
 template <int BM, int BR, int BK, int WM, int WN, bool GATED, int STAGES, bool DENSE = false>
 __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   constexpr int NB = GATED ? 2 : 1;
@@ -280,6 +296,7 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
       if (st < KT) issue(st, st);
   };
 
+  int window_seen = 0;  // the D window word at the last in-tile check (0: closed)
   bf16x8_t fa[2][FM], fb[2][FB];
   auto read_frags = [&](int slot, int sub, bf16x8_t (&a)[FM], bf16x8_t (&b)[FB]) {
     const u32x4* As = &ring[slot][0];
@@ -358,7 +375,18 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
         bare_barrier();
         int ns = slot + 1;
         if (ns == STAGES) ns = 0;
-        if constexpr (MODE == 0) issue(kt + STAGES, slot);
+        if constexpr (MODE == 0) {
+          issue(kt + STAGES, slot);
+          // D first inside a tile: every kPauseEvery slices, a P tile that
+          // found the D window open at the previous check pauses (bounded)
+          // until it closes, so a D layer that starts while long P tiles
+          // run gets the memory bandwidth.  The window word is read one
+          // check ahead, so its load never stalls the pipeline.
+          if (g.yield.word && (kt & (kPauseEvery - 1)) == kPauseEvery - 1) {
+            if (window_seen == g.yield.gen) yield_to_window(g.yield);
+            window_seen = load_untracked(g.yield.word);
+          }
+        }
         read_frags(ns, 0, fa[nxt], fb[nxt]);
         mfmas(fa[cur], fb[cur]);
         interleave<0, NMF, MODE == 0 ? NPS : 0, NRD, 1>();

@@ -92,9 +92,10 @@ __device__ __forceinline__ int block_tile(const G& g) {
 
 // D first (Section 3.1): the planner admits ready D work before P, and a
 // long P execution is cut into segments so that D advances between them
-// (Section 4.2).  On one GPU the segment is a GEMM tile: while the other
-// phase's layer window is open, a workgroup about to start a tile sleeps in
-// steps of 127 * 64 cycles until the window closes, at most `polls` times.
+// (Section 4.2).  On one GPU a segment is a run of K slices of a GEMM tile:
+// while the other phase's layer window is open, a workgroup about to start a
+// tile (and the LDS-ring tiles every few slices, see gemm_ring_body) sleeps
+// in steps of 127 * 64 cycles until the window closes, at most `polls` times.
 // The wait is bounded, so the kernel always finishes, and it is only a hint:
 // no result depends on it.
 __device__ __forceinline__ void yield_to_window(const YieldTo& y) {

@@ -10,9 +10,10 @@ seeded synthetic tensors resident in HBM before timing starts.  Prints one
 JSON line with:
 
 * value: whole-job layer throughput, (T_P + T_D) * K / wall time of K steps;
-* d_latency_us: the D layer's GPU latency (events on the D stream) alone and
-  while P layers keep the other stream busy, p50/p90/p99; graph_*: the same
-  with the D layer captured once into a HIP graph and replayed;
+* d_latency_us: the D layer's GPU latency (events on the D stream) alone
+  (back to back; alone_cold: after clearing the memory-side cache) and while
+  P layers keep the other stream busy, p50/p90/p99; graph_*: the same with
+  the D layer captured once into a HIP graph and replayed;
 * roofline: the kernel with the largest share of GPU time, its algorithmic
   bytes or flops per launch over its mean launch duration, against the MI355X
   peak that bounds it.  Durations come from HIP events recorded around every
@@ -21,10 +22,14 @@ JSON line with:
   without them) with D-first admission off, so that a P kernel's duration is
   its own work and not the waits the admission policy puts in it;
 * D-first admission (--d-priority-us, default 300): while a D layer is in
-  flight, P grouped-GEMM tiles wait for it, up to that bound; value and
-  d_latency_us are measured with it, without_d_first repeats both without;
+  flight, P grouped-GEMM tiles wait for it (at tile starts and every few K
+  slices), up to that bound each time; value and d_latency_us are measured
+  with it, without_d_first repeats both without;
+* engine_clock_mhz: the shader clock, idle and beside P layers (the peaks
+  stay the datasheet's);
 * kernels: mean launch duration of every kernel of both phases;
-* cpu_baseline: the CPU oracle timed on a bounded sample on this host.
+* cpu_baseline: the CPU oracle timed on a bounded sample on this host, with
+  one P pass timed stage by stage and, for the small configs, one thread.
 """
 
 from __future__ import annotations
@@ -151,13 +156,12 @@ def cpu_baseline(inp, seconds):
         if el >= seconds or reps >= 50:
             break
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
 
         threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
     except Exception:  # pragma: no cover - threadpoolctl is optional
-        threads = cores
-    del np
-    return {
+        threads, threadpool_limits = cores, None
+    res = {
         "value": tokens / el,
         "unit": "tokens/s",
         "cores": int(threads),
@@ -165,6 +169,34 @@ def cpu_baseline(inp, seconds):
         "sample": f"{reps} full P ({spec.T_P}) + D ({spec.T_D}) layer passes of the same workload, float64 numpy "
                   f"oracle{' (MX FP8)' if fp8 else ''}, {el:.1f} s",
     }
+    if not fp8:
+        # one P pass, stage by stage (the oracle's own step functions)
+        st = {}
+        t = time.perf_counter()
+        idx, w = oracle.route(inp.logits[0], spec.k)
+        st["route"] = time.perf_counter() - t
+        t = time.perf_counter()
+        le = oracle.local_map(idx, spec.e0, spec.E_loc)
+        counts, offsets, ros, tor = oracle.layout(le, spec.E_loc)
+        st["layout"] = time.perf_counter() - t
+        t = time.perf_counter()
+        xp = oracle.permute(inp.x[0], tor)
+        st["permute"] = time.perf_counter() - t
+        t = time.perf_counter()
+        _, y = oracle.expert_ffn(xp, offsets, inp.w_gu, inp.w_dn)
+        st["ffn"] = time.perf_counter() - t
+        t = time.perf_counter()
+        oracle.combine(y, w, ros, spec.T_P, spec.H)
+        st["combine"] = time.perf_counter() - t
+        res["p_pass_stages_s"] = {kk: round(v, 4) for kk, v in st.items()}
+        if threadpool_limits is not None and spec.T_P * spec.H * spec.I <= 2048 * 2048 * 1024:
+            with threadpool_limits(1):
+                t = time.perf_counter()
+                for ph in (0, 1):
+                    oracle.layer(inp.logits[ph], inp.x[ph], inp.w_gu, inp.w_dn, spec.k, spec.e0)
+                res["one_thread_tokens_per_s"] = (spec.T_P + spec.T_D) / (time.perf_counter() - t)
+    del np
+    return res
 
 
 def copy_calibration(args):
@@ -636,7 +668,18 @@ def main():
         touched[ph] = int((counts > 0).sum())
 
     # ---- D latency alone and under P
-    def d_latencies(under_p, c):
+    # D alone is measured back to back (the layer's weights partly stay in the
+    # 256 MB memory-side cache, as they do under P, whose batch streams the
+    # same weights) and, separately, from a cold cache after a 1 GiB fill
+    # outside the events (a model returns to a layer's weights only after
+    # all its other layers).  The ratio uses the back-to-back figure.
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+
+    def flush_mall():
+        flush.zero_()
+        torch.cuda.current_stream().synchronize()
+
+    def d_latencies(under_p, c, cold=False):
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in
                range(args.d_iters)]
         p_first = torch.cuda.Event(enable_timing=True)
@@ -652,6 +695,8 @@ def main():
             a, b = evs[i]
             if under_p:
                 layer(0, c)  # keep the P stream one layer ahead
+            elif cold:
+                flush_mall()
             a.record(sD)
             layer(1, c)
             b.record(sD)
@@ -667,6 +712,7 @@ def main():
         return lat, overlapped
 
     lat_alone, _ = d_latencies(False, ctx)
+    lat_cold, _ = d_latencies(False, ctx, cold=True)
     lat_under, overlapped = d_latencies(True, ctx)
 
     # ---- the same, with the D layer captured once into a HIP graph and
@@ -704,6 +750,23 @@ def main():
         return res
 
     glat = d_graph_latencies(ctx)
+
+    # the shader clock, idle and beside P layers (peaks stay the datasheet's)
+    def clock_mhz(under_p):
+        buf = torch.zeros(2, dtype=torch.int64, device=dev)
+        sc = torch.cuda.Stream(device=dev)
+        torch.cuda.synchronize()
+        if under_p:
+            for _ in range(3):
+                layer(0, ctx)
+        M.check(M.moe_clock_probe(sc, 400, buf.data_ptr()), "moe_clock_probe")
+        torch.cuda.synchronize()
+        ticks, ref = buf.tolist()
+        return round(ticks * 100.0 / ref, 1)
+
+    clock = {"idle": clock_mhz(False), "beside_p": clock_mhz(True),
+             "note": "shader-clock ticks over a 100 MHz reference-clock spin of 400 us (one wave); "
+                     "beside_p: while P layers run on the P stream"}
     segments = segment_sweep(args, M, ctx, lg, xs, T, spec, sP, dev) if args.seg_layers > 0 else None
     router = None if args.no_router else router_measure(M, ctx_off, xs, T, spec, inp, sP, sD, packed)
     if ctx_off is not ctx:
@@ -766,14 +829,19 @@ def main():
                    "parallelism": "single GPU, P and D on two streams", "d_priority_us": args.d_priority_us},
         "d_latency_us": {
             "p50_alone": round(p50a, 2), "p90_alone": round(pct(lat_alone, 90), 2),
+            "p50_alone_cold": round(pct(lat_cold, 50), 2),
             "p50_under_p": round(p50u, 2), "p90_under_p": round(pct(lat_under, 90), 2),
             "p99_under_p": round(pct(lat_under, 99), 2), "ratio_p50": round(p50u / p50a, 3),
             "iters": args.d_iters, "overlapped_with_p": overlapped,
             "graph_p50_alone": round(pct(glat[False], 50), 2), "graph_p50_under_p": round(pct(glat[True], 50), 2),
             "graph_p90_under_p": round(pct(glat[True], 90), 2),
             "graph_ratio_p50": round(pct(glat[True], 50) / pct(glat[False], 50), 3),
+            "note": "events on the D stream around one D layer; alone: back to back; alone_cold: after a 1 GiB "
+                    "fill that clears the memory-side cache; under_p: with the P stream kept one layer ahead "
+                    "(P streams the same weights)",
         },
         "roofline": roof,
+        "engine_clock_mhz": clock,
         "segments": segments,
         "router_from_hidden": router,
         "kernels": kernels,

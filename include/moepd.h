@@ -311,6 +311,17 @@ int moe_timing_read(moe_ctx_t* ctx, int phase, int kernel, double* total_ms, int
 /* Name of a MOE_KERNEL_* id ("?" when out of range). */
 const char* moe_kernel_name(int kernel);
 
+/* Engine clock probe.  One wave reads the shader-clock counter and the
+ * 100 MHz reference counter, sleeps in short steps until spin_us
+ * microseconds of the reference clock have passed (1..100000), and reads
+ * both again.  out_dev: device memory for two uint64 values, written when
+ * the kernel completes on `stream`: the shader-clock ticks and the
+ * reference ticks of the spin, so the clock in MHz is out[0] * 100 / out[1].
+ * Enqueued beside other work, it reads the clock under that load.  Uses no
+ * context.  Errors: MOE_ERR_INVALID_ARG (null stream or pointer, spin_us
+ * out of range), MOE_ERR_HIP. */
+int moe_clock_probe(hipStream_t stream, int32_t spin_us, uint64_t* out_dev);
+
 #ifdef __cplusplus
 }
 #endif

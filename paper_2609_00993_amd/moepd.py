@@ -142,6 +142,7 @@ _SIGNATURES = {
     "moe_timing_enable": (c_int, [c_void_p, c_int32]),
     "moe_timing_read": (c_int, [c_void_p, c_int, c_int, POINTER(c_double), POINTER(c_int32)]),
     "moe_kernel_name": (c_char_p, [c_int]),
+    "moe_clock_probe": (c_int, [c_void_p, c_int32, c_void_p]),
     "moe_turnstile_create": (c_int, [c_int32, c_int32, POINTER(c_void_p)]),
     "moe_turnstile_destroy": (c_int, [c_void_p]),
     "moe_turnstile_set_span": (c_int, [c_void_p, c_int32]),
@@ -294,6 +295,11 @@ def moe_timing_read(ctx, phase: int, kernel: int):
 
 def moe_kernel_name(kernel: int) -> str:
     return _lib.moe_kernel_name(kernel).decode()
+
+
+def moe_clock_probe(stream, spin_us: int, out_dev) -> int:
+    """out_dev: device buffer of two uint64 (shader-clock ticks, 100 MHz ticks)."""
+    return _lib.moe_clock_probe(_stream(stream), spin_us, _ptr(out_dev))
 
 
 # ---- turnstile (include/moepd_turnstile.h) ----

@@ -124,3 +124,13 @@ def test_p_epoch_runner_validates_before_touching_the_gpu(lib):
         assert q.task == lib.MOE_TS_IDLE and q.epoch == -1  # nothing began
     finally:
         lib.moe_turnstile_destroy(ts)
+
+
+def test_clock_probe_rejects_bad_arguments(lib):
+    """The clock probe validates on the host before any launch (the stream
+    and buffer values below are never used)."""
+    M = lib
+    assert M.moe_clock_probe(None, 100, 16) == M.MOE_ERR_INVALID_ARG  # null stream
+    assert M.moe_clock_probe(16, 100, None) == M.MOE_ERR_INVALID_ARG  # null output
+    assert M.moe_clock_probe(16, 0, 16) == M.MOE_ERR_INVALID_ARG
+    assert M.moe_clock_probe(16, 100001, 16) == M.MOE_ERR_INVALID_ARG

@@ -304,3 +304,22 @@ def test_config_full_size_sampled(cfg):
             check_h_y(got, sub, inp.w_dn, sub["offsets"], spec, f"cfg{cfg} phase {ph} (sampled rows)")
     finally:
         g.close()
+
+
+def test_clock_probe_reads_a_plausible_clock():
+    """The engine clock probe spins for the requested reference time and
+    reports shader-clock ticks that give a clock between 0.2 and 4 GHz."""
+    import torch
+
+    from paper_2609_00993_amd import moepd as M
+
+    buf = torch.zeros(2, dtype=torch.int64, device="cuda")
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    M.check(M.moe_clock_probe(s, 300, buf.data_ptr()), "moe_clock_probe")
+    torch.cuda.synchronize()
+    ticks, ref = buf.tolist()
+    assert ref >= 300 * 100, ref
+    mhz = ticks * 100.0 / ref
+    print(f"[clock] {mhz:.0f} MHz", flush=True)
+    assert 200 <= mhz <= 4000, mhz

@@ -23,7 +23,7 @@ JSON line with:
   its own work and not the waits the admission policy puts in it;
 * D-first admission (--d-priority-us, default 300): while a D layer is in
   flight, P grouped-GEMM tiles wait for it (at tile starts and every few K
-  slices), up to that bound each time; value and d_latency_us are measured
+  slices), up to that bound per tile; value and d_latency_us are measured
   with it, without_d_first repeats both without;
 * engine_clock_mhz: the shader clock, idle and beside P layers (the peaks
   stay the datasheet's);

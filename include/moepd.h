@@ -149,7 +149,8 @@ typedef struct moe_config {
    * start of its moe_route kernel to the start of its moe_combine kernel), a P
    * grouped-GEMM workgroup about to start a tile, or at every fourth K slice
    * of a running tile, waits for the D layer, for at most about this many
-   * microseconds each time.  A scheduling hint only: results are unchanged. */
+   * microseconds per tile in all.  A scheduling hint only: results are
+   * unchanged. */
   int32_t d_priority_us;
 } moe_config_t;
 

@@ -330,7 +330,8 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
 
   const int L = block_tile<DENSE>(g);
   if (L < 0) return;
-  yield_to_window(g.yield);
+  int wait_budget = g.yield.polls;  // shared by the tile's start and in-tile waits
+  yield_to_window(g.yield, wait_budget);
   TileCoord tc;
   if constexpr (DENSE) {
     dense_tile_at(g, L, BM, BN, tc);
@@ -378,12 +379,12 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
         if constexpr (MODE == 0) {
           issue(kt + STAGES, slot);
           // D first inside a tile: every kPauseEvery slices, a P tile that
-          // found the D window open at the previous check pauses (bounded)
-          // until it closes, so a D layer that starts while long P tiles
-          // run gets the memory bandwidth.  The window word is read one
+          // found the D window open at the previous check pauses until it
+          // closes (within the tile's wait budget), so a D layer that starts
+          // while long P tiles run gets the memory bandwidth.  The window word is read one
           // check ahead, so its load never stalls the pipeline.
           if (g.yield.word && (kt & (kPauseEvery - 1)) == kPauseEvery - 1) {
-            if (window_seen == g.yield.gen) yield_to_window(g.yield);
+            if (window_seen == g.yield.gen) yield_to_window(g.yield, wait_budget);
             window_seen = load_untracked(g.yield.word);
           }
         }

@@ -98,12 +98,19 @@ __device__ __forceinline__ int block_tile(const G& g) {
 // in steps of 127 * 64 cycles until the window closes, at most `polls` times.
 // The wait is bounded, so the kernel always finishes, and it is only a hint:
 // no result depends on it.
-__device__ __forceinline__ void yield_to_window(const YieldTo& y) {
+// `budget` (polls left, wave-uniform) is shared by every wait of one tile,
+// so a tile waits at most `polls` sleep steps in all, however long the
+// window stays open.
+__device__ __forceinline__ void yield_to_window(const YieldTo& y, int& budget) {
   if (!y.word) return;
-  for (int i = 0; i < y.polls; ++i) {
+  for (; budget > 0; --budget) {
     if (__hip_atomic_load(y.word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != y.gen) return;
     __builtin_amdgcn_s_sleep(127);
   }
+}
+__device__ __forceinline__ void yield_to_window(const YieldTo& y) {
+  int budget = y.polls;
+  yield_to_window(y, budget);
 }
 
 }  // namespace moepd

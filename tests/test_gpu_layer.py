@@ -168,6 +168,43 @@ def test_abandoned_d_window_is_not_honoured():
         g.close()
 
 
+def test_open_d_window_costs_p_at_most_one_budget_per_tile():
+    """A D window left open (D's route enqueued, the rest of its layer not)
+    holds each P GEMM tile back for at most about d_priority_us in all: the
+    tile-start and in-tile waits share one budget.  At the mid layer each
+    GEMM runs two rounds of tiles, so P's layer may grow by about
+    4 x 100 us; a budget per wait (nine waits per GEMM1 tile, five per
+    GEMM2 tile) would allow about 2.8 ms.  P still gives the oracle's
+    result."""
+    import time
+
+    import torch
+
+    inp = make_config(1)
+    g = GpuLayer(inp, d_priority_us=100)
+    try:
+        M = g.M
+        g.run(0)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        g.run(0)
+        torch.cuda.synchronize()
+        base = time.perf_counter() - t0
+        s = g.streams[1]
+        M.check(M.moe_route(g.ctx, 1, g.logits[1], g.T[1], s))
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        g.run(0)
+        torch.cuda.synchronize()
+        held = time.perf_counter() - t0
+        print(f"[window] P layer {base * 1e6:.0f} us, with D's window open {held * 1e6:.0f} us", flush=True)
+        assert held < base + 1.2e-3, (base, held)
+        check_phase(g, inp, 0)
+        M.check(M.moe_phase_reset(g.ctx, 1))
+    finally:
+        g.close()
+
+
 def test_phase_isolation():
     """Running P never writes D's buffers (and the reverse): both phases own
     disjoint allocations."""

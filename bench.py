@@ -21,7 +21,7 @@ JSON line with:
   steps (the events themselves cost stream time, so the throughput pass runs
   without them) with D-first admission off, so that a P kernel's duration is
   its own work and not the waits the admission policy puts in it;
-* D-first admission (--d-priority-us, default 300): while a D layer is in
+* D-first admission (--d-priority-us, default 500): while a D layer is in
   flight, P grouped-GEMM tiles wait for it (at tile starts and every few K
   slices), up to that bound per tile; value and d_latency_us are measured
   with it, without_d_first repeats both without;
@@ -69,7 +69,7 @@ def parse():
                     help="MoE layers per P epoch and per D iteration in the segment-policy sweep (0: skip it)")
     ap.add_argument("--seg-epochs", type=int, default=2, help="P epochs per policy in the segment-policy sweep")
     ap.add_argument("--no-router", action="store_true", help="skip the router-GEMM timing")
-    ap.add_argument("--d-priority-us", type=int, default=300,
+    ap.add_argument("--d-priority-us", type=int, default=500,
                     help="D-first admission: longest wait of a P GEMM tile for an in-flight D layer (0 = off)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="instead of the layer, time a plain device copy of this many MiB (the reference kernel "

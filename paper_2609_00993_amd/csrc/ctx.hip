@@ -36,7 +36,7 @@ struct Timing {
 struct Phase {
   int state = MOE_STATE_IDLE;
   int T = 0;
-  int regime = 0;  // bf16 tile shape: 0 large batch, 1 small batch
+  int regime = 0;  // tile shape (ffn_bf16_bm / ffn_mx_bm): 0 large batch, 1 small, 2 very large (bf16)
   int bm = 0;
   int chunk_tokens = 1;
   int nchunks = 1;

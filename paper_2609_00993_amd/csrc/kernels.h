@@ -110,9 +110,10 @@ hipError_t launch_combine(const void* y, const float* topk_w, const int32_t* row
                           void* out, WindowSignal close, hipStream_t s);
 
 // Grouped expert FFN.  `regime` picks the tile configuration (0 = large
-// batches, 128-row tiles; 1 = small batches, 32-row weight-streaming tiles;
-// 2 = very large batches, 256-row tiles); ffn_bf16_bm gives its m-tile
-// height, which the place kernel must use for tile_base.
+// batches, 160-row tiles; 1 = small batches, 32-row weight-streaming tiles,
+// one wave of 32 columns each; 2 = very large batches, 256-row tiles);
+// ffn_bf16_bm gives its m-tile height, which the place kernel must use for
+// tile_base.
 int ffn_bf16_bm(int regime);
 hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
                            int e_loc, int H, int I, int max_m_tiles, YieldTo yield, hipStream_t s);

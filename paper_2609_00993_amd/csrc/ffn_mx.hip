@@ -21,8 +21,7 @@
 // rows straight into registers) and, for large batches, 128 x 128 (gate +
 // up) / 128 x 256 tiles staged through a three-slot LDS ring of 128-deep K
 // slices (128 bytes per row, the byte layout of the bf16 ring's 64-deep
-// slices), with the
-// slices' scale bytes staged alongside.
+// slices), with the slices' scale bytes staged alongside.
 #include <type_traits>
 
 #include "common.h"

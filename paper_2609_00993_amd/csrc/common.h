@@ -30,35 +30,30 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
   return l == 0 ? 0ull : (~0ull >> (64 - l));
 }
 
-// One step of a wave maximum over DPP: each lane in the rows ROW_MASK
-// enables takes the larger of its key and the key DPP control CTRL names;
-// the other lanes keep their own.
-template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ uint64_t dpp_max_step(uint64_t v) {
-  const uint32_t lo = uint32_t(v), hi = uint32_t(v >> 32);
-  const uint32_t olo = __builtin_amdgcn_update_dpp(lo, lo, CTRL, ROW_MASK, 0xF, false);
-  const uint32_t ohi = __builtin_amdgcn_update_dpp(hi, hi, CTRL, ROW_MASK, 0xF, false);
-  const uint64_t o = (uint64_t(ohi) << 32) | olo;
-  return o > v ? o : v;
+// Wave-wide maximum / minimum of a 32-bit unsigned value, returned to all
+// lanes (wave-uniform).  Register moves across lanes (DPP), not LDS-routed
+// shuffles: swaps within quads, then rotations by 4 and 8 lanes give every
+// lane its 16-lane row's extremum; two row broadcasts (lane 15 of rows 0
+// and 2 into rows 1 and 3, then lane 31 into rows 2 and 3) leave the wave's
+// on lane 63, which is read out.
+template <bool MAX, int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_step(uint32_t v) {
+  // lanes left out read the extremum's identity (0 / all ones)
+  const uint32_t o = __builtin_amdgcn_update_dpp(MAX ? 0u : 0xffffffffu, v, CTRL, ROW_MASK, 0xF, false);
+  return MAX ? (o > v ? o : v) : (o < v ? o : v);
 }
-
-// Wave-wide maximum of a 64-bit key, returned to all lanes.  Register moves
-// across lanes (DPP) rather than LDS-routed shuffles, so the k selections
-// of the top-k kernel are a short dependent chain: swaps within quads, then
-// rotations by 4 and 8 lanes give every lane its 16-lane row's maximum; two
-// row broadcasts (lane 15 of rows 0 and 2 into rows 1 and 3, then lane 31
-// into rows 2 and 3) leave the wave's maximum on lane 63, which is read out.
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-  v = dpp_max_step<0xB1, 0xF>(v);   // quad_perm [1,0,3,2]
-  v = dpp_max_step<0x4E, 0xF>(v);   // quad_perm [2,3,0,1]
-  v = dpp_max_step<0x124, 0xF>(v);  // row_ror:4
-  v = dpp_max_step<0x128, 0xF>(v);  // row_ror:8
-  v = dpp_max_step<0x142, 0xA>(v);  // row_bcast:15
-  v = dpp_max_step<0x143, 0xC>(v);  // row_bcast:31
-  const uint32_t lo = __builtin_amdgcn_readlane(uint32_t(v), 63);
-  const uint32_t hi = __builtin_amdgcn_readlane(uint32_t(v >> 32), 63);
-  return (uint64_t(hi) << 32) | lo;
+template <bool MAX>
+__device__ __forceinline__ uint32_t wave_extremum_u32(uint32_t v) {
+  v = dpp_step<MAX, 0xB1, 0xF>(v);   // quad_perm [1,0,3,2]
+  v = dpp_step<MAX, 0x4E, 0xF>(v);   // quad_perm [2,3,0,1]
+  v = dpp_step<MAX, 0x124, 0xF>(v);  // row_ror:4
+  v = dpp_step<MAX, 0x128, 0xF>(v);  // row_ror:8
+  v = dpp_step<MAX, 0x142, 0xA>(v);  // row_bcast:15
+  v = dpp_step<MAX, 0x143, 0xC>(v);  // row_bcast:31
+  return __builtin_amdgcn_readlane(v, 63);
 }
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) { return wave_extremum_u32<true>(v); }
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) { return wave_extremum_u32<false>(v); }
 
 // Inclusive wave scan of int32.
 __device__ __forceinline__ int wave_inclusive_scan(int v) {

@@ -7,11 +7,14 @@
 // renormalised softmax restricted to the selected experts.  Ties go to the
 // lower expert id and -0.0 equals +0.0.
 //
-// Each lane holds ceil(E/64) logits as 64-bit keys (orderable logit bits in
-// the high word, inverted expert id in the low word), so one wave-wide
-// maximum gives the next expert of the ordering, ties included.  The k
-// selections take k shuffle reductions; the selected logit of slot j ends on
-// lane j, which then computes and stores its weight.
+// Each lane holds ceil(E/64) logits as 32-bit orderable keys (larger logit,
+// larger key; expert e = lane + 64 i sits in the lane's slot i).  Selection
+// j takes the wave maximum M of the remaining keys, then the wave minimum of
+// the expert ids whose key is M (ties go to the lower id), and retires that
+// expert's key.  Both reductions are 32-bit DPP maxima/minima, full-rate
+// instructions, where one 64-bit (key, id) reduction would take compare and
+// select pairs per step.  The selected logit of slot j ends on lane j, which
+// then computes and stores its weight.
 //
 // After the router GEMM the kernel first forms each logit: the sum of the
 // GEMM's K-split partial products in split order, plus the expert's bias if
@@ -45,7 +48,7 @@ __global__ __launch_bounds__(256) void route_kernel(const float* logits, int T, 
   if (t >= T) return;  // whole wave leaves together
   const float* row = logits + (size_t)t * E;
 
-  uint64_t key[EPL];
+  uint32_t key[EPL];  // 0 = no expert / taken (every finite logit's key is larger)
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     const int e = lane + i * kWave;
@@ -71,24 +74,30 @@ __global__ __launch_bounds__(256) void route_kernel(const float* logits, int T, 
         v = row[e];
       }
     }
-    key[i] = e < E ? ((uint64_t)orderable(v) << 32) | (uint64_t)(0xffffffffu - (uint32_t)e) : 0ull;
+    key[i] = e < E ? orderable(v) : 0u;
   }
 
   float my_l = 0.f, top = 0.f;
   int my_e = 0;
   for (int j = 0; j < k; ++j) {
-    uint64_t best = 0ull;
+    uint32_t m = 0u;
 #pragma unroll
-    for (int i = 0; i < EPL; ++i) best = key[i] > best ? key[i] : best;
-    best = wave_max_u64(best);
+    for (int i = 0; i < EPL; ++i) m = key[i] > m ? key[i] : m;
+    const uint32_t best = wave_max_u32(m);
+    // the lowest expert id holding `best` (slot order is id order)
+    uint32_t cand = 0xffffffffu;
+#pragma unroll
+    for (int i = EPL - 1; i >= 0; --i)
+      if (key[i] == best) cand = (uint32_t)(lane + i * kWave);
+    const uint32_t win = wave_min_u32(cand);
 #pragma unroll
     for (int i = 0; i < EPL; ++i)
-      if (key[i] == best) key[i] = 0ull;
-    const float l = from_orderable((uint32_t)(best >> 32));
+      if ((uint32_t)(lane + i * kWave) == win) key[i] = 0u;
+    const float l = from_orderable(best);
     if (j == 0) top = l;
     if (lane == j) {
       my_l = l;
-      my_e = (int)(0xffffffffu - (uint32_t)best);
+      my_e = (int)win;
     }
   }
 

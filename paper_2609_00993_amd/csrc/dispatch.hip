@@ -83,6 +83,11 @@ __global__ __launch_bounds__(256) void count_kernel(const int32_t* __restrict__ 
   for (int i = tid; i < e_loc; i += 256) cells[i * nchunks + c] = hist[i];
 }
 
+// LDS word of histogram cell i (one pad word after every 32), and the words
+// that n cells take.
+__device__ __host__ __forceinline__ int cix(int i) { return i + (i >> 5); }
+__device__ __host__ __forceinline__ int cell_words(int n) { return n + (n >> 5) + 1; }
+
 __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ topk_idx, int T, int k, int e0,
                                                     int e_loc, int chunk_tokens, int nchunks, int nbits, int bm,
                                                     PhaseBuffers b) {
@@ -90,8 +95,11 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
   // needs only a few KB and can share a CU with a running prefill GEMM),
   // then per-expert bases, running counts and per-wave counts.
   extern __shared__ int lds_dyn[];
+  // The cells sit in LDS with one pad word after every 32 (index cix(i)):
+  // the scan's per-thread runs of consecutive cells and the per-expert reads
+  // at stride nchunks would otherwise fall on one or two of the 64 banks.
   int* cells = lds_dyn;
-  int* base = cells + e_loc * nchunks;
+  int* base = cells + cell_words(e_loc * nchunks);
   int* run = base + e_loc;
   const int ws = e_loc + 1;    // row stride of the per-wave counts
   int* wcnt = run + e_loc + 1;  // [4][e_loc + 1]
@@ -110,17 +118,17 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
   const int n = e_loc * nchunks;  // <= kMaxCells (host guarantees)
   if (nchunks == 1) {
     // one chunk: count its slots here (LDS integer atomics, order-free)
-    for (int i = tid; i < n; i += 256) cells[i] = 0;
+    for (int i = tid; i < n; i += 256) cells[cix(i)] = 0;
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < kLoadBatch; ++j)
-      if (cat0[j] > 0) atomicAdd(&cells[cat0[j] - 1], 1);
+      if (cat0[j] > 0) atomicAdd(&cells[cix(cat0[j] - 1)], 1);
     for (long long sb = s0 + kLoadBatch * 256; sb < s1; sb += kLoadBatch * 256) {
       int cat[kLoadBatch];
       load_cats(topk_idx, sb, s1, e0, e_loc, cat);
 #pragma unroll
       for (int j = 0; j < kLoadBatch; ++j)
-        if (cat[j] > 0) atomicAdd(&cells[cat[j] - 1], 1);
+        if (cat[j] > 0) atomicAdd(&cells[cix(cat[j] - 1)], 1);
     }
   } else {
     // every cell in one round of loads (the count kernel's blocks wrote them
@@ -135,32 +143,32 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
 #pragma unroll
     for (int j = 0; j < kCellLoads; ++j) {
       const int i = j * 256 + tid;
-      if (i < n) cells[i] = v[j];
+      if (i < n) cells[cix(i)] = v[j];
     }
   }
   __syncthreads();
   const int seg = (n + 255) / 256;
   const int lo = min(n, tid * seg), hi = min(n, lo + seg);
   int sum = 0;
-  for (int i = lo; i < hi; ++i) sum += cells[i];
+  for (int i = lo; i < hi; ++i) sum += cells[cix(i)];
   int total;
   int acc = block_exclusive_scan_256(sum, wave_tot, &total);
   __syncthreads();  // every thread has read wave_tot; cells are rewritten below
   for (int i = lo; i < hi; ++i) {
-    const int v = cells[i];
-    cells[i] = acc;
+    const int v = cells[cix(i)];
+    cells[cix(i)] = acc;
     acc += v;
   }
   __syncthreads();
   // e_loc <= kMaxLocalExperts = 256: thread e owns expert e below
-  if (tid < e_loc) base[tid] = cells[tid * nchunks + c];
+  if (tid < e_loc) base[tid] = cells[cix(tid * nchunks + c)];
   if (c == 0) {
     // publish the dispatch shape: counts, offsets, and the m-tile prefix
     // (a block scan of the per-expert m-tile counts)
     int mt = 0;
     if (tid < e_loc) {
-      const int off = cells[tid * nchunks];
-      const int nxt = (tid + 1 < e_loc) ? cells[(tid + 1) * nchunks] : total;
+      const int off = cells[cix(tid * nchunks)];
+      const int nxt = (tid + 1 < e_loc) ? cells[cix((tid + 1) * nchunks)] : total;
       b.offsets[tid] = off;
       b.counts[tid] = nxt - off;
       mt = (nxt - off + bm - 1) / bm;
@@ -277,7 +285,7 @@ hipError_t launch_place(const int32_t* topk_idx, int T, int k, int e0, int e_loc
                         int bm, const PhaseBuffers& b, hipStream_t s) {
   int nbits = 0;
   while ((1 << nbits) <= e_loc) ++nbits;  // categories 0..e_loc
-  const size_t lds = sizeof(int) * ((size_t)e_loc * nchunks + e_loc + 5 * (size_t)(e_loc + 1));
+  const size_t lds = sizeof(int) * ((size_t)cell_words(e_loc * nchunks) + e_loc + 5 * (size_t)(e_loc + 1));
   place_kernel<<<dim3(nchunks), dim3(256), lds, s>>>(topk_idx, T, k, e0, e_loc, chunk_tokens, nchunks, nbits, bm, b);
   return hipGetLastError();
 }

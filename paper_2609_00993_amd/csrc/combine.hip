@@ -5,11 +5,13 @@
 // Section 5: DeepEP's combine returns expert outputs to their tokens)
 // restricted to one GPU.
 //
-// One wave per token: lanes j < k read slot j's row and weight once, the
+// A wave per token (per part of a token's row for small batches, see
+// waves_per_row): lanes j < k read slot j's row and weight once, the
 // resident slots become a wave-uniform bit mask, and each lane then gathers
 // 16-byte vectors of y from exactly the resident rows (row ids and weights
 // are read back as wave-uniform values), so y is read once per row and out
 // written once per token, fully coalesced, with no per-element slot loads.
+// Up to four resident rows are loaded before they are added, in slot order.
 #include "common.h"
 #include "kernels.h"
 
@@ -17,42 +19,65 @@ namespace moepd {
 
 constexpr int kCombVec = 4;  // 16-byte vectors per lane per pass
 
+constexpr int kCombGroup = 4;  // resident rows loaded together
+
 __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ y, const float* __restrict__ topk_w,
                                                       const int32_t* __restrict__ row_of_slot, int T, int k, int nv,
-                                                      u32x4* __restrict__ out, WindowSignal close) {
+                                                      int parts, u32x4* __restrict__ out, WindowSignal close) {
   // The layer's grouped GEMMs are done once this kernel runs: close the window.
   if (close.word && blockIdx.x == 0 && threadIdx.x == 0)
     __hip_atomic_store(close.word, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int wi = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int t = wi / parts, part = wi - t * parts;
   if (t >= T) return;  // whole wave leaves together
   const int lane = threadIdx.x & 63;
   const int r_l = lane < k ? row_of_slot[(size_t)t * k + lane] : -1;
   const float w_l = lane < k ? topk_w[(size_t)t * k + lane] : 0.f;
   const uint64_t resident = __ballot(r_l >= 0);
   u32x4* o = out + (size_t)t * nv;
-  for (int v0 = 0; v0 < nv; v0 += kWave * kCombVec) {
+  constexpr int PASS = kWave * kCombVec;
+  for (int v0 = part * PASS; v0 < nv; v0 += parts * PASS) {
     float acc[kCombVec][4];
 #pragma unroll
     for (int i = 0; i < kCombVec; ++i)
 #pragma unroll
       for (int e = 0; e < 4; ++e) acc[i][e] = 0.f;
     uint64_t m = resident;
-    while (m) {  // resident slots in ascending slot order
-      const int j = __builtin_ctzll(m);
-      m &= m - 1;
-      const int r = __builtin_amdgcn_readlane(r_l, j);
-      const float w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w_l), j));
-      const u32x4* yr = y + (size_t)r * nv;
-      u32x4 a[kCombVec];
+    while (m) {  // resident slots in ascending slot order, up to kCombGroup at a time
+      int r[kCombGroup];
+      float w[kCombGroup];
+      int n = 0;
 #pragma unroll
-      for (int i = 0; i < kCombVec; ++i) {
-        const int v = v0 + i * kWave + lane;
-        if (v < nv) a[i] = yr[v];
+      for (int q = 0; q < kCombGroup; ++q) {
+        r[q] = 0;
+        w[q] = 0.f;
+        if (m) {
+          const int j = __builtin_ctzll(m);
+          m &= m - 1;
+          r[q] = __builtin_amdgcn_readlane(r_l, j);
+          w[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w_l), j));
+          n = q + 1;
+        }
+      }
+      u32x4 a[kCombGroup][kCombVec];
+#pragma unroll
+      for (int q = 0; q < kCombGroup; ++q) {
+        if (q < n) {
+          const u32x4* yr = y + (size_t)r[q] * nv;
+#pragma unroll
+          for (int i = 0; i < kCombVec; ++i) {
+            const int v = v0 + i * kWave + lane;
+            if (v < nv) a[q][i] = yr[v];
+          }
+        }
       }
 #pragma unroll
-      for (int i = 0; i < kCombVec; ++i)
+      for (int q = 0; q < kCombGroup; ++q)
+        if (q < n)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[i][e] += w * __uint_as_float(a[i][e]);
+          for (int i = 0; i < kCombVec; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[i][e] += w[q] * __uint_as_float(a[q][i][e]);
     }
 #pragma unroll
     for (int i = 0; i < kCombVec; ++i) {
@@ -71,8 +96,10 @@ hipError_t launch_combine(const void* y, const float* topk_w, const int32_t* row
                           void* out, WindowSignal close, hipStream_t s) {
   if (T <= 0) return hipSuccess;
   const int nv = H * 4 / 16;
-  combine_kernel<<<dim3((T + 3) / 4), dim3(256), 0, s>>>((const u32x4*)y, topk_w, row_of_slot, T, k, nv,
-                                                          (u32x4*)out, close);
+  const int parts = waves_per_row(T, nv, kCombVec);
+  const long long waves = (long long)T * parts;
+  combine_kernel<<<dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s>>>(
+      (const u32x4*)y, topk_w, row_of_slot, T, k, nv, parts, (u32x4*)out, close);
   return hipGetLastError();
 }
 

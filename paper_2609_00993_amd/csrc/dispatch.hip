@@ -236,7 +236,8 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
   }
 }
 
-// Token-major scatter, one wave per token: lanes j < k read slot j's row, the
+// Token-major scatter, one wave per token (per part of its row for small
+// batches, see waves_per_row): lanes j < k read slot j's row, the
 // resident slots become a wave-uniform bit mask, and each 16-byte vector of
 // x[t] is read once and written to every row t occupies (row ids read back
 // as wave-uniform values).  Tokens with no resident slot are not read, so HBM
@@ -244,16 +245,17 @@ __global__ __launch_bounds__(256) void place_kernel(const int32_t* __restrict__ 
 constexpr int kPermVec = 4;  // 16-byte vectors per lane per pass
 
 __global__ __launch_bounds__(256) void permute_kernel(const u32x4* __restrict__ x, int T, int k, int nv,
-                                                      const int32_t* __restrict__ row_of_slot,
+                                                      int parts, const int32_t* __restrict__ row_of_slot,
                                                       u32x4* __restrict__ x_perm) {
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int wi = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int t = wi / parts, part = wi - t * parts;
   if (t >= T) return;  // whole wave leaves together
   const int lane = threadIdx.x & 63;
   const int r_l = lane < k ? row_of_slot[(size_t)t * k + lane] : -1;
   const uint64_t resident = __ballot(r_l >= 0);
   if (!resident) return;
   const u32x4* xt = x + (size_t)t * nv;
-  for (int v0 = 0; v0 < nv; v0 += kWave * kPermVec) {
+  for (int v0 = part * kWave * kPermVec; v0 < nv; v0 += parts * kWave * kPermVec) {
     u32x4 a[kPermVec];
 #pragma unroll
     for (int i = 0; i < kPermVec; ++i) {
@@ -293,8 +295,11 @@ hipError_t launch_place(const int32_t* topk_idx, int T, int k, int e0, int e_loc
 hipError_t launch_permute(const void* x, int T, int k, int row_bytes, const int32_t* row_of_slot, void* x_perm,
                           hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  permute_kernel<<<dim3((T + 3) / 4), dim3(256), 0, s>>>((const u32x4*)x, T, k, row_bytes / 16, row_of_slot,
-                                                          (u32x4*)x_perm);
+  const int nv = row_bytes / 16;
+  const int parts = waves_per_row(T, nv, kPermVec);
+  const long long waves = (long long)T * parts;
+  permute_kernel<<<dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s>>>((const u32x4*)x, T, k, nv, parts,
+                                                                          row_of_slot, (u32x4*)x_perm);
   return hipGetLastError();
 }
 

@@ -59,12 +59,14 @@ __device__ __forceinline__ uint32_t e4m3_pair(float a, float b) {
 
 // ------------------------------------------------------------------ permute + quantize
 
-// One wave per token.  Lane l takes 16-byte vector v = v0 + l of the bf16 row
+// One wave per token (per part of its row for small batches, see
+// waves_per_row).  Lane l takes 16-byte vector v = v0 + l of the bf16 row
 // (8 values); four consecutive lanes hold one 32-value block.
 __global__ __launch_bounds__(256) void permute_mx_kernel(const u32x4* __restrict__ x, int T, int k, int H,
-                                                         const int32_t* __restrict__ row_of_slot,
+                                                         int parts, const int32_t* __restrict__ row_of_slot,
                                                          uint8_t* __restrict__ codes, uint8_t* __restrict__ scales) {
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int wi = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int t = wi / parts, part = wi - t * parts;
   if (t >= T) return;  // whole wave leaves together
   const int lane = threadIdx.x & 63;
   const int r_l = lane < k ? row_of_slot[(size_t)t * k + lane] : -1;
@@ -72,7 +74,7 @@ __global__ __launch_bounds__(256) void permute_mx_kernel(const u32x4* __restrict
   if (!resident) return;
   const int nv = H / 8, nb = H / 32;
   const u32x4* xt = x + (size_t)t * nv;
-  for (int v0 = 0; v0 < nv; v0 += kWave) {
+  for (int v0 = part * kWave; v0 < nv; v0 += parts * kWave) {
     const int v = v0 + lane;
     const bool on = v < nv;  // nv is a multiple of 4: a block is all on or all off
     float f[8];
@@ -113,7 +115,10 @@ __global__ __launch_bounds__(256) void permute_mx_kernel(const u32x4* __restrict
 hipError_t launch_permute_mx(const void* x, int T, int k, int H, const int32_t* row_of_slot, uint8_t* codes,
                              uint8_t* scales, hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  permute_mx_kernel<<<dim3((T + 3) / 4), dim3(256), 0, s>>>((const u32x4*)x, T, k, H, row_of_slot, codes, scales);
+  const int parts = waves_per_row(T, H / 8, 1);
+  const long long waves = (long long)T * parts;
+  permute_mx_kernel<<<dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s>>>((const u32x4*)x, T, k, H, parts,
+                                                                             row_of_slot, codes, scales);
   return hipGetLastError();
 }
 

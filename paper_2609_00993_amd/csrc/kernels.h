@@ -105,6 +105,16 @@ hipError_t launch_place(const int32_t* topk_idx, int T, int k, int e0, int e_loc
 hipError_t launch_permute(const void* x, int T, int k, int row_bytes, const int32_t* row_of_slot, void* x_perm,
                           hipStream_t s);
 
+// Waves per token row in the permute and combine kernels: one for large
+// batches (the rows alone fill the GPU); for small batches (up to 2048
+// tokens) one per pass of 64 lanes x vec 16-byte vectors, so a token's passes
+// run side by side instead of one after another.
+inline int waves_per_row(int T, int nv, int vec) {
+  if (T > 2048) return 1;
+  const int pass = 64 * vec;
+  return (nv + pass - 1) / pass;
+}
+
 // out[t] = sum_j w[t,j] y[row(t,j)] in float32 (y and out are float32).
 hipError_t launch_combine(const void* y, const float* topk_w, const int32_t* row_of_slot, int T, int k, int H,
                           void* out, WindowSignal close, hipStream_t s);

@@ -54,7 +54,7 @@ struct GemmArgs {
   long long b_stride;
   int e_loc, N, K, n_tiles, up_row;
   int n_group;    // n-tiles per block of the within-expert tile order (see tile_at)
-  int xcd_local;  // 1: consecutive tiles on one XCD (block_tile); 0: dealt round-robin
+  int xcd_local;  // 1: consecutive tiles on one XCD (block_tile); 0: dealt round-robin; 2: striped (tile_at)
   YieldTo yield;  // the other phase's layer window to hold back for, if any
   // Dense mode (the router GEMM): one group of dense_rows rows, no offsets;
   // K is cut into dense_splits runs of dense_ks slices and split s writes its
@@ -519,7 +519,7 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
     constexpr int bn = 32 * kDecodeWaves, threads = 64 * kDecodeWaves;
     g.n_tiles = (g.N + bn - 1) / bn;
     g.n_group = 1;
-    g.xcd_local = 1;
+    g.xcd_local = g.n_tiles % 8 == 0 ? 2 : 1;
     const dim3 grid(round8((long long)max_m_tiles * g.n_tiles));
     const bool rot = g.K % 2048 == 0;
     if (gemm == 1) {

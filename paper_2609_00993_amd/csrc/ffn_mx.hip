@@ -572,6 +572,7 @@ hipError_t launch_ffn_mx(int regime, int gemm, const PhaseBuffers& b, const MxBu
     else gemm2_mx_prefill<<<grid, 256, 0, s>>>(g);
   } else {
     g.n_tiles = (g.N + 32 * kMxDecodeWaves - 1) / (32 * kMxDecodeWaves);
+    g.xcd_local = g.n_tiles % 8 == 0 ? 2 : 1;
     const dim3 grid(round8_mx((long long)max_m_tiles * g.n_tiles));
     if (gemm == 1) gemm_mx_skinny<true><<<grid, 64 * kMxDecodeWaves, 0, s>>>(g);
     else gemm_mx_skinny<false><<<grid, 64 * kMxDecodeWaves, 0, s>>>(g);

@@ -43,6 +43,14 @@ __device__ __forceinline__ void dense_tile_at(const G& g, int L, int bm, int bn,
 // tiles and a short rest) lets them drift apart along K and fetch the panel
 // from HBM again.  Tiles dealt round-robin over the XCDs start at multiples
 // of bm (measured faster for the 256-row tiles, which run that way).
+// Striped tiles (xcd_local == 2, n_tiles a multiple of 8, n_group 1) run
+// in plain block order, so block L runs on XCD L % 8; within an expert,
+// XCD x takes the n-tiles nt = x (mod 8), each with all its m-tiles in a row.
+// Every XCD then streams an eighth of every expert's weights, and the m-tiles
+// of one n-tile still share them in that XCD's L2.  With contiguous ranges per
+// XCD, a skewed batch gives one XCD a single popular expert (many m-tiles,
+// few weight bytes) and another many rare ones (few m-tiles each, many
+// bytes); the tile counts match but the bytes to fetch do not.
 template <class G>
 __device__ __forceinline__ void tile_at(const G& g, int L, int bm, int bn, TileCoord& tc) {
   int lo = 0, hi = g.e_loc - 1;
@@ -54,15 +62,24 @@ __device__ __forceinline__ void tile_at(const G& g, int L, int bm, int bn, TileC
   const int e = lo;
   const int mt_e = g.tile_base[e + 1] - g.tile_base[e];
   const int local = L - g.tile_base[e] * g.n_tiles;
-  const int b = g.n_group;
-  const int full = g.n_tiles / b;  // full n-blocks; a narrower one may follow
-  int blk = local / (mt_e * b), bw = b, r;
-  if (blk >= full) {
-    blk = full;
-    bw = g.n_tiles - full * b;
+  int mt, nt;
+  if (g.xcd_local == 2) {
+    const int j = local >> 3;
+    const int q = j / mt_e;
+    mt = j - q * mt_e;
+    nt = 8 * q + (local & 7);
+  } else {
+    const int b = g.n_group;
+    const int full = g.n_tiles / b;  // full n-blocks; a narrower one may follow
+    int blk = local / (mt_e * b), bw = b;
+    if (blk >= full) {
+      blk = full;
+      bw = g.n_tiles - full * b;
+    }
+    const int r = local - blk * mt_e * b;
+    mt = r / bw;
+    nt = blk * b + (r - mt * bw);
   }
-  r = local - blk * mt_e * b;
-  const int mt = r / bw, nt = blk * b + (r - mt * bw);
   const int beg = g.offsets[e], rows = g.offsets[e + 1] - beg;
   const int per = g.xcd_local ? (rows + mt_e - 1) / mt_e : bm;
   tc.e = e;
@@ -82,7 +99,7 @@ __device__ __forceinline__ int block_tile(const G& g) {
   int total;
   if constexpr (DENSE) total = g.dense_total;
   else total = g.tile_base[g.e_loc] * g.n_tiles;
-  if (!g.xcd_local) return (int)blockIdx.x < total ? (int)blockIdx.x : -1;
+  if (g.xcd_local != 1) return (int)blockIdx.x < total ? (int)blockIdx.x : -1;
   const int per_xcd = (total + 7) >> 3;
   const int slot = blockIdx.x >> 3;
   if (slot >= per_xcd) return -1;

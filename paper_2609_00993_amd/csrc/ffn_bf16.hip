@@ -95,20 +95,47 @@ constexpr int kDecodeWaves = 1;
 
 template <bool GATED, bool ROT>
 __device__ __forceinline__ void gemm_skinny_tile(const GemmArgs& g, const TileCoord& tc) {
+  static_assert(kDecodeWaves == 1, "the LDS stage below is private to the workgroup's one wave");
   constexpr int BN = 32 * kDecodeWaves;
   constexpr int NB = GATED ? 2 : 1;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r = lane & 31, kg = lane >> 5;
-  const int arow = min(tc.m0 + r, tc.m_end - 1);
-  const int col = tc.n0 + wave * 32 + r;
-  const int colc = min(col, g.N - 1);
+  constexpr int NP = 1 + NB;  // panels: the tile's activation rows, then its weight rows (gate, up)
+  // A 64-deep K block of one panel is 32 rows x 128 B.  It is loaded as four
+  // 1 KB instructions that each read eight whole 128-byte row pieces (lane
+  // l: row 8i + l/8, 16-byte chunk l%8): reading 16 bytes from each of 32
+  // rows per instruction, as the MFMA lane layout would, reaches only about a
+  // quarter of the per-CU rate of whole-line reads.  The block then goes
+  // through this wave's LDS stage, chunk c of row r at slot 8r + (c ^ r%8)
+  // (no bank conflicts on either side), and is read back in the MFMA layout.
+  __shared__ u32x4 stage[NP][32 * 8];
+  const int lane = threadIdx.x & 63;
+  const int lr = lane >> 3, lc = lane & 7;  // coalesced side: row within eight, chunk
+  const int r = lane & 31, kg = lane >> 5;  // MFMA side
+  const int col = tc.n0 + r;
   const uint16_t* Be = g.B + (size_t)tc.e * g.b_stride;
+  const u32x4* base[NP];
+  base[0] = reinterpret_cast<const u32x4*>(g.A);
+  base[1] = reinterpret_cast<const u32x4*>(Be);
+  if (GATED) base[NP - 1] = reinterpret_cast<const u32x4*>(Be + (size_t)g.up_row * g.K);
+  const int kv = g.K / 8;  // 16-byte chunks per row
+  // Chunk offset of this lane's row piece in block 0.  32 bits suffice: the
+  // decode regime holds fewer than 32 rows per expert on average, so under
+  // 32 x 1024 rows of at most 2048 chunks, and weight panels hold at most
+  // 2 x 16384 rows.
+  int off[NP][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int rr = 8 * i + lr;
+    off[0][i] = min(tc.m0 + rr, tc.m_end - 1) * kv + lc;
+    const int cc = min(tc.n0 + rr, g.N - 1) * kv + lc;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) off[1 + j][i] = cc;
+  }
+  const int wslot = lr * 8 + (lc ^ lr);
   // lane group kg holds k in [64*kb + 32*kg, +32) as four 16-byte chunks;
   // MFMA step s takes chunk s of both groups (the same k map for A and B).
-  const u32x4* pa = reinterpret_cast<const u32x4*>(g.A + (size_t)arow * g.K) + kg * 4;
-  const u32x4* pb[NB];
-  pb[0] = reinterpret_cast<const u32x4*>(Be + (size_t)colc * g.K) + kg * 4;
-  if (GATED) pb[NB - 1] = reinterpret_cast<const u32x4*>(Be + (size_t)(g.up_row + colc) * g.K) + kg * 4;
+  int rslot[4];
+#pragma unroll
+  for (int st = 0; st < 4; ++st) rslot[st] = r * 8 + ((4 * kg + st) ^ (r & 7));
 
   f32x16_t acc[NB];
 #pragma unroll
@@ -119,33 +146,40 @@ __device__ __forceinline__ void gemm_skinny_tile(const GemmArgs& g, const TileCo
   const int KB = g.K / 64;
   const int krot = ROT ? k_rotation(tc, g.n_tiles, BN, KB) : 0;
   constexpr int PF = 2;  // 64-deep K blocks in flight per wave (a static register ring)
-  u32x4 ra[PF][4], rb[PF][NB][4];
-  auto load = [&](int kb, u32x4 (&a)[4], u32x4 (&b)[NB][4]) {
+  u32x4 v[PF][NP][4];
+  auto load = [&](int kb, u32x4 (&d)[NP][4]) {
     if (ROT) {
       kb += krot;
       if (kb >= KB) kb -= KB;
     }
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      a[s] = pa[kb * 8 + s];
+    for (int p = 0; p < NP; ++p)
 #pragma unroll
-      for (int j = 0; j < NB; ++j) b[j][s] = pb[j][kb * 8 + s];
-    }
+      for (int i = 0; i < 4; ++i) d[p][i] = base[p][off[p][i] + kb * 8];
   };
 #pragma unroll
-  for (int p = 0; p < PF; ++p)
-    if (p < KB) load(p, ra[p], rb[p]);
+  for (int q = 0; q < PF; ++q)
+    if (q < KB) load(q, v[q]);
   for (int kb0 = 0; kb0 < KB; kb0 += PF) {
 #pragma unroll
-    for (int p = 0; p < PF; ++p) {
-      const int kb = kb0 + p;
+    for (int q = 0; q < PF; ++q) {
+      const int kb = kb0 + q;
       if (kb < KB) {
+        // LDS operations of one wave run in order, so these writes land after
+        // the previous block's reads and before this block's.
 #pragma unroll
-        for (int s = 0; s < 4; ++s)
+        for (int p = 0; p < NP; ++p)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) stage[p][64 * i + wslot] = v[q][p][i];
+        if (kb + PF < KB) load(kb + PF, v[q]);
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+          const u32x4 a = stage[0][rslot[st]];
 #pragma unroll
           for (int j = 0; j < NB; ++j)
-            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(ra[p][s]), as_bf16x8(rb[p][j][s]), acc[j], 0, 0, 0);
-        if (kb + PF < KB) load(kb + PF, ra[p], rb[p]);
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(stage[1 + j][rslot[st]]), acc[j],
+                                                            0, 0, 0);
+        }
       }
     }
   }

@@ -150,33 +150,68 @@ __device__ __forceinline__ float silu_mul_mx(float gt, float up) {
   return gt * __builtin_amdgcn_rcpf(1.f + __expf(-gt)) * up;
 }
 
+// Small batches: one wave (32 output columns) per workgroup, so that the
+// tiles spread evenly over the CUs whatever their count (with four-wave
+// workgroups, 1.5 tiles per CU left half the CUs with two).
+constexpr int kMxDecodeWaves = 1;
+
 // One wave: 32 output columns x 32 rows of the tile, over all of K.  The
 // MFMAs take the weight rows as their first operand, so lane l ends with
 // token row l % 32 and the 16 columns 8q + 4h + (0..3), q = 0..3.
+// A 128-deep K block of a panel (the tile's 32 code rows, or its 32 gate or
+// up weight rows) is 4 KB: it is loaded by four 1 KB whole-line reads (lane
+// l: row 8i + l/8, 16-byte unit l%8), written to this wave's LDS stage (unit
+// c of row r at slot 8r + (c ^ r%8), no bank conflicts either way) and read
+// back in the MFMA lane layout; reading 16 bytes from each of 32 rows per
+// instruction reaches only about a quarter of the per-CU rate of whole-line
+// reads.  A row's four scale bytes of the block come as one 4-byte load.
 template <bool GATED>
 __device__ __forceinline__ void gemm_mx_skinny_tile(const GemmArgsMX& g, const TileCoord& tc) {
+  static_assert(kMxDecodeWaves == 1, "the LDS stage below is private to the workgroup's one wave");
   constexpr int NB = GATED ? 2 : 1;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int NP = 1 + NB;  // panels: code rows, then weight rows (gate, up)
+  __shared__ u32x4 stage[NP][32 * 8];
+  const int lane = threadIdx.x & 63;
   const int r = lane & 31, h = lane >> 5;
-  const int col0 = tc.n0 + wave * 32;
+  const int lr = lane >> 3, lc = lane & 7;
+  const int col0 = tc.n0;
   if (col0 >= g.N) return;  // N is a multiple of 32: a wave's columns are all in or all out
-  const int arow = min(tc.m0 + r, tc.m_end - 1);
-  const int wrow = col0 + r;
   const int KS = g.K / 32;
   const uint8_t* Be = g.B + (size_t)tc.e * g.b_stride;
   const uint8_t* Bse = g.Bs + (size_t)tc.e * g.bs_stride;
-  // 16-byte units of a row; a 128-deep K block is 8 units, the lane takes
-  // units 2p + h of each 64-deep step (p = 0, 1)
-  const u32x4* pa = reinterpret_cast<const u32x4*>(g.A + (size_t)arow * g.K) + h;
-  const uint8_t* psa = g.As + (size_t)arow * KS + h;
-  const u32x4* pb[NB];
-  const uint8_t* psb[NB];
-  pb[0] = reinterpret_cast<const u32x4*>(Be + (size_t)wrow * g.K) + h;
-  psb[0] = Bse + (size_t)wrow * KS + h;
+  const u32x4* base[NP];
+  const uint32_t* sbase[NP];
+  base[0] = reinterpret_cast<const u32x4*>(g.A);
+  sbase[0] = reinterpret_cast<const uint32_t*>(g.As);
+  base[1] = reinterpret_cast<const u32x4*>(Be);
+  sbase[1] = reinterpret_cast<const uint32_t*>(Bse);
   if (GATED) {
-    pb[NB - 1] = reinterpret_cast<const u32x4*>(Be + (size_t)(g.up_row + wrow) * g.K) + h;
-    psb[NB - 1] = Bse + (size_t)(g.up_row + wrow) * KS + h;
+    base[NP - 1] = reinterpret_cast<const u32x4*>(Be + (size_t)g.up_row * g.K);
+    sbase[NP - 1] = reinterpret_cast<const uint32_t*>(Bse + (size_t)g.up_row * KS);
   }
+  // Offsets in 16-byte units and scale words; 32 bits suffice (fewer than
+  // 32 x 1024 code rows of at most 1024 units in this regime, at most
+  // 2 x 16384 weight rows).
+  const int kv = g.K / 16, kw = KS / 4;
+  int off[NP][4], soff[NP];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int rr = 8 * i + lr;
+    off[0][i] = min(tc.m0 + rr, tc.m_end - 1) * kv + lc;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) off[1 + j][i] = (col0 + rr) * kv + lc;
+  }
+  soff[0] = min(tc.m0 + r, tc.m_end - 1) * kw;
+#pragma unroll
+  for (int j = 0; j < NB; ++j) soff[1 + j] = (col0 + r) * kw;
+  const int wslot = lr * 8 + (lc ^ lr);
+  // Step s (64 deep) of a block: lane (r, h) holds units 4s + h and 4s + 2 + h
+  // of its row and the scale of 32-value block 2s + h.
+  int rslot[2][2];
+#pragma unroll
+  for (int st = 0; st < 2; ++st)
+#pragma unroll
+    for (int u = 0; u < 2; ++u) rslot[st][u] = r * 8 + ((4 * st + 2 * u + h) ^ (r & 7));
 
   f32x16_mx acc[NB];
 #pragma unroll
@@ -186,38 +221,44 @@ __device__ __forceinline__ void gemm_mx_skinny_tile(const GemmArgsMX& g, const T
 
   const int KB = g.K / 128;
   constexpr int PF = 2;  // 128-deep K blocks in flight per wave
-  u32x4 ra[PF][4], rb[PF][NB][4];
-  int sa[PF][2], sb[PF][NB][2];
-  auto load = [&](int kb, u32x4 (&a)[4], u32x4 (&b)[NB][4], int (&ssa)[2], int (&ssb)[NB][2]) {
+  u32x4 v[PF][NP][4];
+  uint32_t sc[PF][NP];
+  auto load = [&](int kb, u32x4 (&d)[NP][4], uint32_t (&ds)[NP]) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      a[u] = pa[kb * 8 + 2 * u];
+    for (int p = 0; p < NP; ++p) {
 #pragma unroll
-      for (int j = 0; j < NB; ++j) b[j][u] = pb[j][kb * 8 + 2 * u];
-    }
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      ssa[s] = psa[kb * 4 + 2 * s];
-#pragma unroll
-      for (int j = 0; j < NB; ++j) ssb[j][s] = psb[j][kb * 4 + 2 * s];
+      for (int i = 0; i < 4; ++i) d[p][i] = base[p][off[p][i] + kb * 8];
+      ds[p] = sbase[p][soff[p] + kb];
     }
   };
 #pragma unroll
-  for (int p = 0; p < PF; ++p)
-    if (p < KB) load(p, ra[p], rb[p], sa[p], sb[p]);
+  for (int q = 0; q < PF; ++q)
+    if (q < KB) load(q, v[q], sc[q]);
   for (int kb0 = 0; kb0 < KB; kb0 += PF) {
 #pragma unroll
-    for (int p = 0; p < PF; ++p) {
-      const int kb = kb0 + p;
+    for (int q = 0; q < PF; ++q) {
+      const int kb = kb0 + q;
       if (kb < KB) {
+        // LDS operations of one wave run in order, so these writes land after
+        // the previous block's reads and before this block's.
 #pragma unroll
-        for (int s = 0; s < 2; ++s)
+        for (int p = 0; p < NP; ++p)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) stage[p][64 * i + wslot] = v[q][p][i];
+        uint32_t scl[NP];
+#pragma unroll
+        for (int p = 0; p < NP; ++p) scl[p] = sc[q][p] >> (8 * h);
+        if (kb + PF < KB) load(kb + PF, v[q], sc[q]);
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+          const v8i32 a = join(stage[0][rslot[st][0]], stage[0][rslot[st][1]]);
+          const int sa = (int)((scl[0] >> (16 * st)) & 0xffu);
 #pragma unroll
           for (int j = 0; j < NB; ++j)
             acc[j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                join(rb[p][j][2 * s], rb[p][j][2 * s + 1]), join(ra[p][2 * s], ra[p][2 * s + 1]), acc[j], 0, 0, 0,
-                sb[p][j][s], 0, sa[p][s]);
-        if (kb + PF < KB) load(kb + PF, ra[p], rb[p], sa[p], sb[p]);
+                join(stage[1 + j][rslot[st][0]], stage[1 + j][rslot[st][1]]), a, acc[j], 0, 0, 0,
+                (int)((scl[1 + j] >> (16 * st)) & 0xffu), 0, sa);
+        }
       }
     }
   }
@@ -513,11 +554,6 @@ __global__ __launch_bounds__(256) void gemm1_mx_prefill(GemmArgsMX g) {
 __global__ __launch_bounds__(256) void gemm2_mx_prefill(GemmArgsMX g) {
   gemm_mx_ring_body<128, 256, 2, 2, false, 3>(g);
 }
-
-// Small batches: one wave (32 output columns) per workgroup, so that the
-// tiles spread evenly over the CUs whatever their count (with four-wave
-// workgroups, 1.5 tiles per CU left half the CUs with two).
-constexpr int kMxDecodeWaves = 1;
 
 template <bool GATED>
 __global__ __launch_bounds__(64 * kMxDecodeWaves) void gemm_mx_skinny(GemmArgsMX g) {

@@ -11,6 +11,7 @@
 // admits one pending operation at a time and moves through explicit states
 // (Section 5.2); a reset is refused until the phase's enqueued work is done
 // (Section 5.3).
+#include <atomic>
 #include <new>
 #include <string.h>
 
@@ -65,6 +66,13 @@ struct moe_ctx {
   int device;
   int esz;
   Phase ph[MOE_NUM_PHASES];
+  // Tile regime of each phase's latest bf16 expert-FFN launch (-1: none).
+  // The other phase reads it (possibly from another host thread) to choose
+  // its decode tiles: 160-row prefill tiles leave 4 KB of a CU's LDS free,
+  // too little for the LDS-staged decode tile, so beside them the phase takes
+  // the tile that needs no LDS and can share their CUs.  Only a performance
+  // choice: both tiles give the same results.
+  std::atomic<int> ffn_regime[MOE_NUM_PHASES] = {-1, -1};
 };
 
 namespace {
@@ -456,6 +464,8 @@ int moe_expert_ffn(moe_ctx_t* ctx, int phase, hipStream_t stream) {
     const int kk = c.top_k < c.num_local_experts ? c.top_k : c.num_local_experts;
     const long long rows = (long long)p.T * kk;
     const int max_m_tiles = (int)((rows + p.bm - 1) / p.bm) + c.num_local_experts;
+    ctx->ffn_regime[phase].store(p.regime, std::memory_order_relaxed);
+    const bool stage = ctx->ffn_regime[phase ^ 1].load(std::memory_order_relaxed) != 0;
     for (int gemm = 1; gemm <= 2; ++gemm) {
       st = timed(p, gemm == 1 ? MOE_KERNEL_GEMM1 : MOE_KERNEL_GEMM2, stream, [&] {
         if (c.dtype == MOE_DTYPE_FP8)
@@ -464,7 +474,7 @@ int moe_expert_ffn(moe_ctx_t* ctx, int phase, hipStream_t stream) {
                                c.num_local_experts, c.hidden, c.inter, max_m_tiles, yield_of(ctx, phase), stream);
         if (c.dtype == MOE_DTYPE_BF16)
           return launch_ffn_bf16(p.regime, gemm, p.b, ctx->w.w_gate_up, ctx->w.w_down, c.num_local_experts, c.hidden,
-                                 c.inter, max_m_tiles, yield_of(ctx, phase), stream);
+                                 c.inter, max_m_tiles, stage, yield_of(ctx, phase), stream);
         return launch_ffn_f32(gemm, p.b, ctx->w.w_gate_up, ctx->w.w_down, c.num_local_experts, c.hidden, c.inter,
                               max_m_tiles, stream);
       });

@@ -198,7 +198,82 @@ __device__ __forceinline__ void gemm_skinny_tile(const GemmArgs& g, const TileCo
   }
 }
 
+// The same tile with each operand loaded straight into MFMA lane layout (16
+// bytes from each of 32 rows per instruction) and no LDS: slower alone, but
+// it fits on a CU beside a 160-row prefill tile of the other phase, whose
+// ring leaves 4 KB of LDS free.
 template <bool GATED, bool ROT>
+__device__ __forceinline__ void gemm_skinny_tile_direct(const GemmArgs& g, const TileCoord& tc) {
+  constexpr int BN = 32 * kDecodeWaves;
+  constexpr int NB = GATED ? 2 : 1;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 31, kg = lane >> 5;
+  const int arow = min(tc.m0 + r, tc.m_end - 1);
+  const int col = tc.n0 + wave * 32 + r;
+  const int colc = min(col, g.N - 1);
+  const uint16_t* Be = g.B + (size_t)tc.e * g.b_stride;
+  // lane group kg holds k in [64*kb + 32*kg, +32) as four 16-byte chunks;
+  // MFMA step s takes chunk s of both groups (the same k map for A and B).
+  const u32x4* pa = reinterpret_cast<const u32x4*>(g.A + (size_t)arow * g.K) + kg * 4;
+  const u32x4* pb[NB];
+  pb[0] = reinterpret_cast<const u32x4*>(Be + (size_t)colc * g.K) + kg * 4;
+  if (GATED) pb[NB - 1] = reinterpret_cast<const u32x4*>(Be + (size_t)(g.up_row + colc) * g.K) + kg * 4;
+
+  f32x16_t acc[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[j][q] = 0.f;
+
+  const int KB = g.K / 64;
+  const int krot = ROT ? k_rotation(tc, g.n_tiles, BN, KB) : 0;
+  constexpr int PF = 2;  // 64-deep K blocks in flight per wave (a static register ring)
+  u32x4 ra[PF][4], rb[PF][NB][4];
+  auto load = [&](int kb, u32x4 (&a)[4], u32x4 (&b)[NB][4]) {
+    if (ROT) {
+      kb += krot;
+      if (kb >= KB) kb -= KB;
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      a[s] = pa[kb * 8 + s];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) b[j][s] = pb[j][kb * 8 + s];
+    }
+  };
+#pragma unroll
+  for (int p = 0; p < PF; ++p)
+    if (p < KB) load(p, ra[p], rb[p]);
+  for (int kb0 = 0; kb0 < KB; kb0 += PF) {
+#pragma unroll
+    for (int p = 0; p < PF; ++p) {
+      const int kb = kb0 + p;
+      if (kb < KB) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(ra[p][s]), as_bf16x8(rb[p][j][s]), acc[j], 0, 0, 0);
+        if (kb + PF < KB) load(kb + PF, ra[p], rb[p]);
+      }
+    }
+  }
+
+  if (col < g.N) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int row = tc.m0 + acc_row(q, lane);
+      if (row < tc.m_end) {
+        if (GATED)
+          static_cast<uint16_t*>(g.C)[(size_t)row * g.N + col] = f32_to_bf16(silu_mul(acc[0][q], acc[NB - 1][q]));
+        else
+          static_cast<float*>(g.C)[(size_t)row * g.N + col] = acc[0][q];
+      }
+    }
+  }
+}
+
+template <bool GATED, bool ROT, bool STAGE>
 __device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
   constexpr int BM = 32, BN = 32 * kDecodeWaves;
   const int L = block_tile(g);
@@ -206,7 +281,8 @@ __device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
   yield_to_window(g.yield);
   TileCoord tc;
   tile_at(g, L, BM, BN, tc);
-  gemm_skinny_tile<GATED, ROT>(g, tc);
+  if constexpr (STAGE) gemm_skinny_tile<GATED, ROT>(g, tc);
+  else gemm_skinny_tile_direct<GATED, ROT>(g, tc);
 }
 
 // One workgroup of 4 waves computes a BM x BN output tile of one expert.
@@ -495,10 +571,14 @@ __global__ __launch_bounds__(256) void gemm2_down_prefill(GemmArgs g) { gemm_rin
 __global__ __launch_bounds__(256) void router_gemm(GemmArgs g) { gemm_ring_body<64, 128, 64, 2, 2, false, 3, true>(g); }
 __global__ __launch_bounds__(256) void gemm1_swiglu_wide(GemmArgs g) { gemm_ring_body<256, 256, 32, 2, 2, true, 4>(g); }
 __global__ __launch_bounds__(256) void gemm2_down_wide(GemmArgs g) { gemm_ring_body<256, 256, 32, 2, 2, false, 4>(g); }
-template <bool ROT>
-__global__ __launch_bounds__(64 * kDecodeWaves) void gemm1_swiglu_decode(GemmArgs g) { gemm_skinny<true, ROT>(g); }
-template <bool ROT>
-__global__ __launch_bounds__(64 * kDecodeWaves) void gemm2_down_decode(GemmArgs g) { gemm_skinny<false, ROT>(g); }
+template <bool ROT, bool STAGE>
+__global__ __launch_bounds__(64 * kDecodeWaves) void gemm1_swiglu_decode(GemmArgs g) {
+  gemm_skinny<true, ROT, STAGE>(g);
+}
+template <bool ROT, bool STAGE>
+__global__ __launch_bounds__(64 * kDecodeWaves) void gemm2_down_decode(GemmArgs g) {
+  gemm_skinny<false, ROT, STAGE>(g);
+}
 
 // ------------------------------------------------------------------ launch
 
@@ -507,7 +587,7 @@ int ffn_bf16_bm(int regime) { return regime == 0 ? 160 : regime == 2 ? 256 : 32;
 static inline int round8(long long v) { return (int)((v + 7) / 8 * 8); }
 
 hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
-                           int e_loc, int H, int I, int max_m_tiles, YieldTo yield, hipStream_t s) {
+                           int e_loc, int H, int I, int max_m_tiles, bool stage, YieldTo yield, hipStream_t s) {
   GemmArgs g;
   g.yield = yield;
   g.offsets = b.offsets;
@@ -556,12 +636,13 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
     g.xcd_local = g.n_tiles % 8 == 0 ? 2 : 1;
     const dim3 grid(round8((long long)max_m_tiles * g.n_tiles));
     const bool rot = g.K % 2048 == 0;
+    auto go = [&](auto k) { k<<<grid, threads, 0, s>>>(g); };
     if (gemm == 1) {
-      if (rot) gemm1_swiglu_decode<true><<<grid, threads, 0, s>>>(g);
-      else gemm1_swiglu_decode<false><<<grid, threads, 0, s>>>(g);
+      if (stage) rot ? go(gemm1_swiglu_decode<true, true>) : go(gemm1_swiglu_decode<false, true>);
+      else rot ? go(gemm1_swiglu_decode<true, false>) : go(gemm1_swiglu_decode<false, false>);
     } else {
-      if (rot) gemm2_down_decode<true><<<grid, threads, 0, s>>>(g);
-      else gemm2_down_decode<false><<<grid, threads, 0, s>>>(g);
+      if (stage) rot ? go(gemm2_down_decode<true, true>) : go(gemm2_down_decode<false, true>);
+      else rot ? go(gemm2_down_decode<true, false>) : go(gemm2_down_decode<false, false>);
     }
   }
   return hipGetLastError();

@@ -125,8 +125,11 @@ hipError_t launch_combine(const void* y, const float* topk_w, const int32_t* row
 // ffn_bf16_bm gives its m-tile height, which the place kernel must use for
 // tile_base.
 int ffn_bf16_bm(int regime);
+// stage (decode regime only): load operands as whole lines through a per-wave
+// LDS stage (faster), or straight into registers with no LDS, so the tiles fit
+// on CUs held by the other phase's 160-row prefill tiles.
 hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
-                           int e_loc, int H, int I, int max_m_tiles, YieldTo yield, hipStream_t s);
+                           int e_loc, int H, int I, int max_m_tiles, bool stage, YieldTo yield, hipStream_t s);
 
 // MX FP8 contexts: the phase's x_perm and h regions hold E4M3 codes
 // followed by their E8M0 scale bytes (one per 32 values of a row).

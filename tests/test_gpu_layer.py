@@ -205,6 +205,29 @@ def test_open_d_window_costs_p_at_most_one_budget_per_tile():
         g.close()
 
 
+@pytest.mark.parametrize("name", ["cfg1-mid-bf16", "ragged-bf16"])
+def test_decode_tiles_staged_and_direct_bit_identical(name):
+    """D's decode tiles load their operands through an LDS stage, except
+    while the other phase's latest FFN ran 160-row prefill tiles (they leave
+    too little LDS), when they load straight into registers.  D alone takes
+    the first, D after such a P the second: both must give the same bits
+    (same MFMAs in the same order) and match the oracle."""
+    inp = SPECS[name]()
+    g = GpuLayer(inp)
+    try:
+        g.run(1)  # P has not run: staged decode tiles
+        staged = _snapshot(g, 1)
+        check_phase(g, inp, 1)
+        g.run(0)  # P on 160-row tiles
+        g.run(1)  # direct decode tiles
+        direct = _snapshot(g, 1)
+        for key in staged:
+            assert np.array_equal(staged[key], direct[key]), key
+        check_phase(g, inp, 1)
+    finally:
+        g.close()
+
+
 def test_phase_isolation():
     """Running P never writes D's buffers (and the reverse): both phases own
     disjoint allocations."""

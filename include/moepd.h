@@ -266,7 +266,11 @@ int moe_dispatch_permute(moe_ctx_t* ctx, int phase, const void* x, hipStream_t s
  * contexts multiply bf16 operands with float32 accumulation, round h to bf16
  * (nearest even; h is GEMM2's operand) and keep y in float32; float32
  * contexts compute everything in float32.  The tile schedule
- * is read from the device-side offsets (no host synchronisation).
+ * is read from the device-side offsets (no host synchronisation).  bf16
+ * small-batch tiles come in two forms with identical results: LDS-staged,
+ * or, when the other phase's latest moe_expert_ffn ran large-batch tiles
+ * (which leave too little LDS to share their CUs), register-direct; a
+ * captured graph keeps the form chosen at capture.
  * Errors: MOE_ERR_INVALID_ARG, MOE_ERR_INVALID_PHASE, MOE_ERR_STATE, MOE_ERR_HIP. */
 int moe_expert_ffn(moe_ctx_t* ctx, int phase, hipStream_t stream);
 

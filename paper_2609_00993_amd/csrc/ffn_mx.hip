@@ -165,7 +165,11 @@ constexpr int kMxDecodeWaves = 1;
 // back in the MFMA lane layout; reading 16 bytes from each of 32 rows per
 // instruction reaches only about a quarter of the per-CU rate of whole-line
 // reads.  A row's four scale bytes of the block come as one 4-byte load.
-template <bool GATED>
+// SC2 (K a multiple of 256, scale arrays 8-byte aligned): a row's scale
+// bytes of two blocks come as one 8-byte load every second block.  Scale
+// loads read a few bytes from each of 32 rows per instruction (the slow
+// pattern), so halving them leaves the whole-line code loads more room.
+template <bool GATED, bool SC2>
 __device__ __forceinline__ void gemm_mx_skinny_tile(const GemmArgsMX& g, const TileCoord& tc) {
   static_assert(kMxDecodeWaves == 1, "the LDS stage below is private to the workgroup's one wave");
   constexpr int NB = GATED ? 2 : 1;
@@ -222,43 +226,60 @@ __device__ __forceinline__ void gemm_mx_skinny_tile(const GemmArgsMX& g, const T
   const int KB = g.K / 128;
   constexpr int PF = 2;  // 128-deep K blocks in flight per wave
   u32x4 v[PF][NP][4];
+  auto mfma_block = [&](const uint32_t (&scl)[NP]) {
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      const v8i32 a = join(stage[0][rslot[st][0]], stage[0][rslot[st][1]]);
+      const int sa = (int)((scl[0] >> (16 * st)) & 0xffu);
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        acc[j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+            join(stage[1 + j][rslot[st][0]], stage[1 + j][rslot[st][1]]), a, acc[j], 0, 0, 0,
+            (int)((scl[1 + j] >> (16 * st)) & 0xffu), 0, sa);
+    }
+  };
+  // LDS operations of one wave run in order, so a block's stage writes land
+  // after the previous block's reads and before its own.
+  auto stage_block = [&](const u32x4 (&d)[NP][4]) {
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) stage[p][64 * i + wslot] = d[p][i];
+  };
+  // Scale words of the block pair in flight (SC2) or of each block.
+  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
   uint32_t sc[PF][NP];
+  u32x2 sp[NP], sp_next[NP];
   auto load = [&](int kb, u32x4 (&d)[NP][4], uint32_t (&ds)[NP]) {
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) d[p][i] = base[p][off[p][i] + kb * 8];
-      ds[p] = sbase[p][soff[p] + kb];
+      if (SC2) {
+        if ((kb & 1) == 0) sp_next[p] = *reinterpret_cast<const u32x2*>(sbase[p] + soff[p] + kb);
+      } else {
+        ds[p] = sbase[p][soff[p] + kb];
+      }
     }
   };
 #pragma unroll
   for (int q = 0; q < PF; ++q)
     if (q < KB) load(q, v[q], sc[q]);
   for (int kb0 = 0; kb0 < KB; kb0 += PF) {
+    if (SC2) {
+#pragma unroll
+      for (int p = 0; p < NP; ++p) sp[p] = sp_next[p];
+    }
 #pragma unroll
     for (int q = 0; q < PF; ++q) {
       const int kb = kb0 + q;
       if (kb < KB) {
-        // LDS operations of one wave run in order, so these writes land after
-        // the previous block's reads and before this block's.
-#pragma unroll
-        for (int p = 0; p < NP; ++p)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) stage[p][64 * i + wslot] = v[q][p][i];
+        stage_block(v[q]);
         uint32_t scl[NP];
 #pragma unroll
-        for (int p = 0; p < NP; ++p) scl[p] = sc[q][p] >> (8 * h);
+        for (int p = 0; p < NP; ++p) scl[p] = (SC2 ? sp[p][q] : sc[q][p]) >> (8 * h);
         if (kb + PF < KB) load(kb + PF, v[q], sc[q]);
-#pragma unroll
-        for (int st = 0; st < 2; ++st) {
-          const v8i32 a = join(stage[0][rslot[st][0]], stage[0][rslot[st][1]]);
-          const int sa = (int)((scl[0] >> (16 * st)) & 0xffu);
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-            acc[j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                join(stage[1 + j][rslot[st][0]], stage[1 + j][rslot[st][1]]), a, acc[j], 0, 0, 0,
-                (int)((scl[1 + j] >> (16 * st)) & 0xffu), 0, sa);
-        }
+        mfma_block(scl);
       }
     }
   }
@@ -555,14 +576,14 @@ __global__ __launch_bounds__(256) void gemm2_mx_prefill(GemmArgsMX g) {
   gemm_mx_ring_body<128, 256, 2, 2, false, 3>(g);
 }
 
-template <bool GATED>
+template <bool GATED, bool SC2>
 __global__ __launch_bounds__(64 * kMxDecodeWaves) void gemm_mx_skinny(GemmArgsMX g) {
   const int L = block_tile(g);
   if (L < 0) return;
   yield_to_window(g.yield);
   TileCoord tc;
   tile_at(g, L, 32, 32 * kMxDecodeWaves, tc);
-  gemm_mx_skinny_tile<GATED>(g, tc);
+  gemm_mx_skinny_tile<GATED, SC2>(g, tc);
 }
 
 static inline int round8_mx(long long v) { return (int)((v + 7) / 8 * 8); }
@@ -610,8 +631,11 @@ hipError_t launch_ffn_mx(int regime, int gemm, const PhaseBuffers& b, const MxBu
     g.n_tiles = (g.N + 32 * kMxDecodeWaves - 1) / (32 * kMxDecodeWaves);
     g.xcd_local = g.n_tiles % 8 == 0 ? 2 : 1;
     const dim3 grid(round8_mx((long long)max_m_tiles * g.n_tiles));
-    if (gemm == 1) gemm_mx_skinny<true><<<grid, 64 * kMxDecodeWaves, 0, s>>>(g);
-    else gemm_mx_skinny<false><<<grid, 64 * kMxDecodeWaves, 0, s>>>(g);
+    const bool sc2 = g.K % 256 == 0 && ((uintptr_t)g.As | (uintptr_t)g.Bs) % 8 == 0 && g.bs_stride % 8 == 0 &&
+                     ((long long)g.up_row * (g.K / 32)) % 8 == 0;
+    auto go = [&](auto k) { k<<<grid, 64 * kMxDecodeWaves, 0, s>>>(g); };
+    if (gemm == 1) sc2 ? go(gemm_mx_skinny<true, true>) : go(gemm_mx_skinny<true, false>);
+    else sc2 ? go(gemm_mx_skinny<false, true>) : go(gemm_mx_skinny<false, false>);
   }
   return hipGetLastError();
 }

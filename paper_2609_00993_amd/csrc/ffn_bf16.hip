@@ -28,10 +28,12 @@
 //    mostly empty m-tile that ceil(rows / 128) adds whenever an expert holds
 //    a little more than 256 rows, and every m-tile re-streams the weights;
 //  * small batches (decode, a few rows per expert): the layer is a weight
-//    stream, so each wave reads its weight rows straight into MFMA operand
-//    registers (no LDS round trip), one 32-row m-tile and 32 columns per
-//    single-wave workgroup, with the next two 64-deep K blocks in flight
-//    while one is multiplied.
+//    stream, one 32-row m-tile and 32 columns per single-wave workgroup,
+//    two 64-deep K blocks in flight.  Each block is loaded with whole-line
+//    reads and transposed through the wave's own 12 KB LDS stage into MFMA
+//    operand layout; beside the other phase's 160-row prefill tiles (which
+//    leave 4 KB of LDS) the tile loads straight into operand registers
+//    instead, with no LDS, so it can share their CUs.
 #include <type_traits>
 
 #include "common.h"

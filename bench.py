@@ -28,8 +28,12 @@ JSON line with:
 * engine_clock_mhz: the shader clock, idle and beside P layers (the peaks
   stay the datasheet's);
 * kernels: mean launch duration of every kernel of both phases;
-* cpu_baseline: the CPU oracle timed on a bounded sample on this host, with
-  one P pass timed stage by stage and, for the small configs, one thread.
+* cpu_baseline: the CPU oracle timed on this host on a bounded, seeded sample
+  of the same workload (a subset of each phase's tokens, at most 4096 P
+  tokens and the same fraction of the D batch; the whole batch when it is
+  smaller), its P pass timed stage by stage and, for the small configs, one
+  thread; cores = the BLAS threads it ran with (the host's CPU share, at most
+  the CPUs this process may run on, which are reported beside it).
 """
 
 from __future__ import annotations
@@ -58,12 +62,14 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=1,
-                    help="workload id (0..7); 1 is the headline workload, 4 the agentic trace on the config-2 layer, "
-                         "5 the config-2 layer in MX FP8, 6/7 the paper's model shape in FP8/BF16")
+    ap.add_argument("--config", type=int, default=3,
+                    help="workload id (0..7); 3 (the skewed DeepSeek-V3-shaped share, the largest one-GPU workload) "
+                         "is the headline, 4 the agentic trace on the config-2 layer, 5 the config-2 layer in MX FP8, "
+                         "6/7 the paper's model shape in FP8/BF16")
     ap.add_argument("--trace-steps", type=int, default=200, help="steps of the agentic trace (config 4)")
     ap.add_argument("--d-iters", type=int, default=60, help="D layers per latency measurement")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="least time of the CPU-oracle sample")
+    ap.add_argument("--cpu-tokens", type=int, default=4096, help="P tokens in the CPU-oracle sample (at most)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seg-layers", type=int, default=40,
                     help="MoE layers per P epoch and per D iteration in the segment-policy sweep (0: skip it)")
@@ -131,71 +137,103 @@ def recorded_traffic(cfg, phase, kernel):
         return None
 
 
-def cpu_baseline(inp, seconds):
+def cpu_threads():
+    """BLAS threads for the CPU oracle: the host's CPU share (OMP_NUM_THREADS,
+    else 16), never more than the CPUs this process may run on."""
+    affinity = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    try:
+        share = int(os.environ.get("OMP_NUM_THREADS", "16"))
+    except ValueError:
+        share = 16
+    return max(1, min(affinity, share)), affinity
+
+
+def cpu_baseline(inp, seconds, max_p_tokens):
+    """The oracle as it stands, timed on a seeded sample of the workload's
+    tokens: each phase's sub-batch runs the whole layer (route, layout,
+    permute, expert FFN, combine); a token's output depends on no other
+    token, so the sample is the same work per token as the full batch.
+    Passes repeat until `seconds` have elapsed (at least one)."""
     import numpy as np
 
     import oracle
 
     spec = inp.spec
-    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
-    tokens, reps = 0, 0
-    t0 = time.perf_counter()
+    threads, affinity = cpu_threads()
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        threadpool_limits = None
+    rng = np.random.default_rng(7)
+    T = {0: spec.T_P, 1: spec.T_D}
+    n_p = min(T[0], max_p_tokens)
+    n = {0: n_p, 1: min(T[1], max(1, round(T[1] * n_p / max(T[0], 1))))}
+    toks = {ph: np.sort(rng.choice(T[ph], size=n[ph], replace=False)) for ph in (0, 1)}
     fp8 = inp.w_gu_scales is not None
     if fp8:
         from oracle import mx as oracle_mx
-    while True:
-        for ph in (0, 1):
-            if fp8:
-                oracle_mx.layer_mx(inp.logits[ph], inp.x[ph], inp.w_gu_bits, inp.w_gu_scales, inp.w_dn_bits,
-                                   inp.w_dn_scales, spec.k, spec.e0)
-            else:
-                oracle.layer(inp.logits[ph], inp.x[ph], inp.w_gu, inp.w_dn, spec.k, spec.e0)
-            tokens += (spec.T_P, spec.T_D)[ph]
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds or reps >= 50:
-            break
-    try:
-        from threadpoolctl import threadpool_info, threadpool_limits
 
-        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover - threadpoolctl is optional
-        threads, threadpool_limits = cores, None
-    res = {
-        "value": tokens / el,
-        "unit": "tokens/s",
-        "cores": int(threads),
-        "kind": "oracle",
-        "sample": f"{reps} full P ({spec.T_P}) + D ({spec.T_D}) layer passes of the same workload, float64 numpy "
-                  f"oracle{' (MX FP8)' if fp8 else ''}, {el:.1f} s",
-    }
-    if not fp8:
-        # one P pass, stage by stage (the oracle's own step functions)
+    stages = {}
+
+    def one_pass(ph):
+        lg, x = inp.logits[ph][toks[ph]], inp.x[ph][toks[ph]]
+        if fp8:
+            oracle_mx.layer_mx(lg, x, inp.w_gu_bits, inp.w_gu_scales, inp.w_dn_bits, inp.w_dn_scales, spec.k, spec.e0)
+            return
+        # oracle.layer's steps, each timed (the P pass's times are reported)
         st = {}
         t = time.perf_counter()
-        idx, w = oracle.route(inp.logits[0], spec.k)
+        idx, w = oracle.route(lg, spec.k)
         st["route"] = time.perf_counter() - t
         t = time.perf_counter()
         le = oracle.local_map(idx, spec.e0, spec.E_loc)
         counts, offsets, ros, tor = oracle.layout(le, spec.E_loc)
         st["layout"] = time.perf_counter() - t
         t = time.perf_counter()
-        xp = oracle.permute(inp.x[0], tor)
+        xp = oracle.permute(x, tor)
         st["permute"] = time.perf_counter() - t
         t = time.perf_counter()
         _, y = oracle.expert_ffn(xp, offsets, inp.w_gu, inp.w_dn)
         st["ffn"] = time.perf_counter() - t
         t = time.perf_counter()
-        oracle.combine(y, w, ros, spec.T_P, spec.H)
+        oracle.combine(y, w, ros, n[ph], spec.H)
         st["combine"] = time.perf_counter() - t
-        res["p_pass_stages_s"] = {kk: round(v, 4) for kk, v in st.items()}
-        if threadpool_limits is not None and spec.T_P * spec.H * spec.I <= 2048 * 2048 * 1024:
-            with threadpool_limits(1):
-                t = time.perf_counter()
-                for ph in (0, 1):
-                    oracle.layer(inp.logits[ph], inp.x[ph], inp.w_gu, inp.w_dn, spec.k, spec.e0)
-                res["one_thread_tokens_per_s"] = (spec.T_P + spec.T_D) / (time.perf_counter() - t)
-    del np
+        if ph == 0 and not stages:
+            stages.update(st)
+
+    import contextlib
+
+    limit = threadpool_limits(threads) if threadpool_limits is not None else contextlib.nullcontext()
+    with limit:
+        tokens, reps = 0, 0
+        t0 = time.perf_counter()
+        while True:
+            for ph in (0, 1):
+                if n[ph]:
+                    one_pass(ph)
+                    tokens += n[ph]
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= seconds or reps >= 50:
+                break
+    res = {
+        "value": tokens / el,
+        "unit": "tokens/s",
+        "cores": int(threads),
+        "affinity_cpus": int(affinity),
+        "kind": "oracle",
+        "sample": f"{reps} pass(es) of the float64 numpy oracle{' (MX FP8)' if fp8 else ''} over a seeded sample "
+                  f"of {n[0]} of the {T[0]} P tokens and {n[1]} of the {T[1]} D tokens of the same workload "
+                  f"(the whole layer per sub-batch), {el:.1f} s on {threads} BLAS threads",
+    }
+    if stages:
+        res["p_pass_stages_s"] = {kk: round(v, 4) for kk, v in stages.items()}
+    if threadpool_limits is not None and not fp8 and spec.T_P * spec.H * spec.I <= 2048 * 2048 * 1024:
+        with threadpool_limits(1):
+            t = time.perf_counter()
+            for ph in (0, 1):
+                oracle.layer(inp.logits[ph], inp.x[ph], inp.w_gu, inp.w_dn, spec.k, spec.e0)
+            res["one_thread_tokens_per_s"] = (spec.T_P + spec.T_D) / (time.perf_counter() - t)
     return res
 
 
@@ -860,7 +898,7 @@ def main():
     if ctx_off is not ctx:
         M.check(M.moe_ctx_destroy(ctx_off))
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds, args.cpu_tokens)
     print(json.dumps(res), flush=True)
 
 

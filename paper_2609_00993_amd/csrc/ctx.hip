@@ -156,7 +156,9 @@ int alloc_phase(moe_ctx* ctx, int phase) {
   p.router_cap = c.dtype != MOE_DTYPE_F32 ? (p.max_tokens > 4096 ? p.max_tokens : 4096) : 0;
   const size_t o_lg = take((size_t)p.max_tokens * c.num_experts * 4);
   const size_t o_part = take((size_t)p.router_cap * c.num_experts * 4);
-  const size_t o_cc = take((size_t)E * mc * 4), o_tb = take((E + 1) * 4), o_sig = take(4);
+  // The signal slot is 16 bytes: the grouped GEMMs read the window word in it
+  // with a 16-byte LDS DMA (its other words stay zero).
+  const size_t o_cc = take((size_t)E * mc * 4), o_tb = take((E + 1) * 4), o_sig = take(16);
 
   void* mem = nullptr;
   if (hipMalloc(&mem, off) != hipSuccess || !mem) {

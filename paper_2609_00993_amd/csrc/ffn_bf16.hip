@@ -317,18 +317,31 @@ __device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
 // Slices between the in-tile checks of the D window (a power of two).
 constexpr int kPauseEvery = 4;
 
-// The D window word, read device-coherently by a load the compiler does not
-// track.  A tracked load read a check later made the compiler wait for every
-// outstanding operation (it cannot follow the count through the loop),
-// draining the DMA ring.  Untracked, it is one extra operation after the
-// slice's DMA: the ring's counted waits then wait for one more (a little
-// early, never late), and two slice waits later the load has completed;
-// its value is read kPauseEvery slices later.  It only steers a pause.
-__device__ __forceinline__ int load_untracked(const int32_t* word) {
+// The D window word is read one check ahead by an LDS DMA issued after a
+// slice's DMA: every lane lands the 16 bytes that start at the word (the
+// phase's signal slot is 16 bytes) in its own 16-byte cell of one array the
+// four waves share; all cells then hold a copy of the word.  The DMA is one
+// more operation in the ring's queue: the counted waits at the slice ends
+// retire it with the slices issued before the next one (waiting for one
+// operation more than the slices need, never one less), so it has landed two
+// slice ends later, and it is read back from LDS at the next check,
+// kPauseEvery slices on.  A register load would either make the compiler
+// wait for every outstanding DMA before its use (it cannot follow the count
+// through the loop) or, untracked, leave a register the compiler may reuse
+// while the load is still in flight.  Waves of one tile that read a cell while
+// another wave's next DMA lands in it see the older or the newer copy; the
+// word only steers a pause, and no result depends on it.  The LDS read is
+// written out (with its own wait for LDS results) because the compiler,
+// which tracks the 4-word DMA into this array, would otherwise wait for
+// every outstanding DMA before it, draining the ring at each check; the
+// counted waits have already retired the DMA it reads.
+__device__ __forceinline__ int read_window_cell(const void* cell) {
+  const uint32_t a = (uint32_t)(uintptr_t)MOEPD_LPTR(cell);
   int v;
-  asm volatile("global_load_dword %0, %1, off sc1" : "=v"(v) : "v"(word) : "memory");
+  asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(a) : "memory");
   return v;
 }
+constexpr int kCachePolicyAgent = 0x10;  // sc1: coherent at agent scope
 
 template <int BM, int BR, int BK, int WM, int WN, bool GATED, int STAGES, bool DENSE = false>
 __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
@@ -349,7 +362,14 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   static_assert(A_INS * RPI * 4 == BM && B_INS * RPI * 4 == BR, "slices split into whole DMA instructions");
   static_assert(FM * 32 == WTM && FN * 32 == WTN, "wave tile must be a multiple of 32x32");
   static_assert(STAGES >= 2 && NPS * (STAGES - 1) < 64, "pipeline depth");
-  __shared__ u32x4 ring[STAGES][A_CH + B_CH];
+  // One LDS object: the ring of K slices, then the cells of the D window
+  // word (its first word in each cell, see load_window).
+  struct Lds {
+    u32x4 ring[STAGES][A_CH + B_CH];
+    u32x4 window[64];
+  };
+  __shared__ Lds lds;
+  auto& ring = lds.ring;
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -401,14 +421,18 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
       __builtin_amdgcn_global_load_lds(MOEPD_GPTR(b_src[i] + koff),
                                        MOEPD_LPTR(&ring[slot][A_CH + (wave * B_INS + i) * 64]), 16, 0, 0);
   };
+  auto load_window = [&] {
+    __builtin_amdgcn_global_load_lds(MOEPD_GPTR(g.yield.word), MOEPD_LPTR(&lds.window[0]), 16, 0,
+                                     kCachePolicyAgent);
+  };
   auto prologue = [&](const TileCoord& tc) {
     set_sources(tc);
 #pragma unroll
     for (int st = 0; st < STAGES; ++st)
       if (st < KT) issue(st, st);
+    if (g.yield.word) load_window();
   };
 
-  int window_seen = 0;  // the D window word at the last in-tile check (0: closed)
   bf16x8_t fa[2][FM], fb[2][FB];
   auto read_frags = [&](int slot, int sub, bf16x8_t (&a)[FM], bf16x8_t (&b)[FB]) {
     const u32x4* As = &ring[slot][0];
@@ -491,13 +515,16 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
         if constexpr (MODE == 0) {
           issue(kt + STAGES, slot);
           // D first inside a tile: every kPauseEvery slices, a P tile that
-          // found the D window open at the previous check pauses until it
-          // closes (within the tile's wait budget), so a D layer that starts
-          // while long P tiles run gets the memory bandwidth.  The window word is read one
-          // check ahead, so its load never stalls the pipeline.
+          // found the D window open at the previous check (or at the tile's
+          // start) pauses until it closes (within the tile's wait budget), so
+          // a D layer that starts while long P tiles run gets the memory
+          // bandwidth.  The word read here was loaded into LDS one check
+          // ahead, so its load never stalls the pipeline; its LDS read
+          // completes before the next load into the same words is issued.
           if (g.yield.word && (kt & (kPauseEvery - 1)) == kPauseEvery - 1) {
-            if (window_seen == g.yield.gen) yield_to_window(g.yield, wait_budget);
-            window_seen = load_untracked(g.yield.word);
+            const int seen = __builtin_amdgcn_readfirstlane(read_window_cell(&lds.window[lane]));
+            if (seen == g.yield.gen) yield_to_window(g.yield, wait_budget);
+            load_window();
           }
         }
         read_frags(ns, 0, fa[nxt], fb[nxt]);

@@ -24,7 +24,8 @@ struct PhaseBuffers {
   int32_t* tile_base;     // [E_loc + 1], prefix sum of m-tiles per expert
   // Signal word of this phase's layer window: a generation number while a
   // layer is between its route and its combine, 0 otherwise.  Written only
-  // by this phase's kernels; read by the other phase's grouped GEMMs.
+  // by this phase's kernels; read by the other phase's grouped GEMMs.  It is
+  // the first word of a zeroed 16-byte slot (read as one 16-byte vector).
   int32_t* signal;
   // router GEMM (moe_route_from_hidden)
   float* logits;    // [Tmax, E] float32, the logits top-k selects from

@@ -209,3 +209,74 @@ def assert_close_rms(got, ref, tol, what=""):
     scale = rms(ref)
     err = float(np.max(np.abs(got - ref)))
     assert err <= tol * scale, f"{what}: max|err| {err:.3e} > {tol:g} x rms {scale:.3e}"
+
+
+def covering_rows(offsets, stride: int = 32) -> np.ndarray:
+    """Rows that cover every m-tile of every expert segment: each segment's
+    first row, every stride-th row after it, the row just before each of
+    those, and its last row.  Any tile of at least `stride` rows that starts
+    at a segment's start or at a multiple of at least `stride` rows into it
+    (all the GEMMs' tile shapes: 32-row decode tiles, 160-row tiles with the
+    rows shared evenly, 256-row tiles) holds one of them, and so does each
+    expert's ragged tail.  Sorted, so the rows stay grouped by expert."""
+    off = np.asarray(offsets, np.int64)
+    rows = []
+    for e in range(len(off) - 1):
+        a, b = int(off[e]), int(off[e + 1])
+        if a == b:
+            continue
+        r = np.arange(a, b, stride)
+        rows.append(r)
+        rows.append(np.maximum(r - 1, a))
+        rows.append(np.minimum(r + stride - 1, b - 1))
+        rows.append(np.array([b - 1]))
+    if not rows:
+        return np.zeros(0, np.int64)
+    return np.unique(np.concatenate(rows))
+
+
+def sub_offsets(rows, offsets) -> np.ndarray:
+    """Offsets of the experts' segments within a sorted subset of rows."""
+    return np.searchsorted(np.asarray(rows), np.asarray(offsets, np.int64)).astype(np.int64)
+
+
+def check_rows_h_y(res, inp, ph, rows, offsets, token_of_row, what=""):
+    """h and y of a subset of rows (sorted, so grouped by expert) against the
+    oracle's expert FFN on the same rows, element by element (check_h_y's
+    bounds).  A row's h and y depend only on its own x row and expert."""
+    import oracle
+
+    spec = inp.spec
+    so = sub_offsets(rows, offsets)
+    xr = inp.x[ph][np.asarray(token_of_row)[rows]]
+    h_ref, y_ref = oracle.expert_ffn(xr, so, inp.w_gu, inp.w_dn)
+    got = dict(h=res["h"][rows], y=res["y"][rows])
+    check_h_y(got, dict(h=h_ref, y=y_ref), inp.w_dn, so, spec, what)
+
+
+def sample_tokens(T: int, row_tokens, n_uniform: int, n_rows: int, seed: int):
+    """A seeded uniform sample of tokens (its output RMS stands for the whole
+    phase's) and a seeded sample of the tokens that own covering rows."""
+    rng = np.random.default_rng(seed)
+    uni = np.sort(rng.choice(T, size=min(T, n_uniform), replace=False))
+    own = np.unique(np.asarray(row_tokens))
+    if own.size > n_rows:
+        own = np.sort(rng.choice(own, size=n_rows, replace=False))
+    return uni, own
+
+
+def check_out_sampled(res, inp, ph, uni, own, tol, what=""):
+    """The layer output of sampled tokens against the oracle run on the
+    sampled sub-batch (a token's output depends on no other token).  The bar
+    is tol x the RMS of the oracle's output over the uniform sample, an
+    unbiased stand-in for the RMS over the whole phase batch."""
+    import oracle
+
+    spec = inp.spec
+    toks = np.union1d(uni, own)
+    sub = oracle.layer(inp.logits[ph][toks], inp.x[ph][toks], inp.w_gu, inp.w_dn, spec.k, spec.e0)
+    scale = rms(sub["out"][np.searchsorted(toks, uni)])
+    got = np.asarray(res["out"][toks], np.float64)
+    err = float(np.max(np.abs(got - sub["out"]))) if toks.size else 0.0
+    assert err <= tol * scale, f"{what}: max|err| {err:.3e} > {tol:g} x rms {scale:.3e} ({toks.size} tokens)"
+    return err / scale if scale else 0.0

@@ -10,6 +10,7 @@ import pytest
 
 from synth import make_config
 from tests.gpu_util import GpuLayer
+from tests.test_gpu_layer import check_phase
 
 pytestmark = pytest.mark.gpu
 
@@ -65,6 +66,10 @@ def test_d_layer_graph_replays_match_eager(d_priority_us):
         got = _d_state(g)
         for key in ref:
             assert np.array_equal(got[key], ref[key]), ("concurrent", key)
+        # the replayed D layer (every stage) and the eager P layer beside it
+        # against the oracle
+        check_phase(g, inp, 1)
+        check_phase(g, inp, 0)
         # the eager API still works on the phase after the replays
         g.run(1, stream=sg)
         torch.cuda.synchronize()

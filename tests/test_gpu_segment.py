@@ -15,9 +15,10 @@ import time
 import numpy as np
 import pytest
 
+import oracle
 from oracle import turnstile as O
 from synth import BF16, LayerSpec, make_layer
-from tests.gpu_util import GpuLayer, to_dev
+from tests.gpu_util import GpuLayer, assert_close_rms, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -53,8 +54,20 @@ def setup():
     g.run(1)
     torch.cuda.synchronize()
     d_ref = g.out[1].clone()
+    # the oracle's outputs of every P layer (each layer's own hidden rows and
+    # logits, the context's weights) and of the D batch
+    global ORACLE_P, ORACLE_D
+    ORACLE_P = [oracle.layer(p.logits[0], p.x[0], base.w_gu, base.w_dn, SPEC.k, SPEC.e0)["out"] for p in per]
+    ORACLE_D = oracle.layer(base.logits[1], base.x[1], base.w_gu, base.w_dn, SPEC.k, SPEC.e0)["out"]
+    for l in range(LAYERS):
+        assert_close_rms(solo[l].cpu().numpy(), ORACLE_P[l], TOL, f"P layer {l} back to back")
+    assert_close_rms(d_ref.cpu().numpy(), ORACLE_D, TOL, "D layer")
     yield g, xs, lg, solo, d_ref
     g.close()
+
+
+TOL = 2e-2  # bf16 layers: max|err| <= 2e-2 x RMS of the oracle's output
+ORACLE_P, ORACLE_D = None, None
 
 
 def _events(M, ts):
@@ -138,8 +151,10 @@ def test_segmented_epoch_matches_back_to_back(setup, K, d_enqueued):
     torch.cuda.synchronize()
     for l in range(LAYERS):
         assert torch.equal(outs[l], solo[l]), f"layer {l}"
-    for o in d_outs:
+        assert_close_rms(outs[l].cpu().numpy(), ORACLE_P[l], TOL, f"segmented P layer {l}")
+    for i, o in enumerate(d_outs):
         assert torch.equal(o, d_ref)
+        assert_close_rms(o.cpu().numpy(), ORACLE_D, TOL, f"D layer let in at boundary {i}")
     assert M.moe_phase_view(ctx, 0)[1].state == M.MOE_STATE_IDLE
 
 

@@ -647,12 +647,15 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
     // 160-row tiles (a few m-tiles per expert): the m-tiles of one n-tile
     // run together on one XCD and share its weights in that XCD's L2.
     // 256-row tiles (large experts, many m-tiles): tiles are dealt to the
-    // XCDs round-robin, so the whole GPU works through one expert at a time
-    // and the expert's weights stay in the memory-side cache; GEMM1 takes
-    // blocks of four n-tiles so a row block is shared by the tiles in flight.
-    g.n_group = regime == 2 ? (gemm == 1 ? 4 : g.n_tiles) : 1;
-    g.xcd_local = regime == 2 ? 0 : 1;
-    const dim3 grid(round8((long long)max_m_tiles * g.n_tiles));
+    // XCDs in groups (block_tile), so the whole GPU works through one expert
+    // at a time and the expert's bytes stay in the memory-side cache, while
+    // each XCD takes blocks of 8 m-tiles x 4 n-tiles whose row blocks and
+    // weight panels its L2 shares.
+    g.n_group = regime == 2 ? 4 : 1;
+    g.xcd_local = regime == 2 ? 3 : 1;
+    const long long tiles = (long long)max_m_tiles * g.n_tiles;
+    const dim3 grid(regime == 2 ? (int)((tiles + 8 * kXcdGroup - 1) / (8 * kXcdGroup) * (8 * kXcdGroup))
+                                : round8(tiles));
     if (regime == 0) {
       if (gemm == 1) gemm1_swiglu_prefill<<<grid, 256, 0, s>>>(g);
       else gemm2_down_prefill<<<grid, 256, 0, s>>>(g);

@@ -41,8 +41,9 @@ __device__ __forceinline__ void dense_tile_at(const G& g, int L, int bm, int bn,
 // and none is empty): the m-tiles that stream one weight panel on one XCD
 // then move at one pace and keep meeting in L2, where an uneven split (full
 // tiles and a short rest) lets them drift apart along K and fetch the panel
-// from HBM again.  Tiles dealt round-robin over the XCDs start at multiples
-// of bm (measured faster for the 256-row tiles, which run that way).
+// from HBM again.  Tiles dealt round-robin or in groups over the XCDs start
+// at multiples of bm (measured faster for the 256-row tiles, which run that
+// way).
 // Striped tiles (xcd_local == 2, n_tiles a multiple of 8, n_group 1) run
 // in plain block order, so block L runs on XCD L % 8; within an expert,
 // XCD x takes the n-tiles nt = x (mod 8), each with all its m-tiles in a row.
@@ -81,7 +82,7 @@ __device__ __forceinline__ void tile_at(const G& g, int L, int bm, int bn, TileC
     nt = blk * b + (r - mt * bw);
   }
   const int beg = g.offsets[e], rows = g.offsets[e + 1] - beg;
-  const int per = g.xcd_local ? (rows + mt_e - 1) / mt_e : bm;
+  const int per = (g.xcd_local == 1 || g.xcd_local == 2) ? (rows + mt_e - 1) / mt_e : bm;
   tc.e = e;
   tc.m0 = beg + mt * per;
   tc.m_end = min(tc.m0 + per, beg + rows);
@@ -94,11 +95,31 @@ __device__ __forceinline__ void tile_at(const G& g, int L, int bm, int bn, TileC
 // [x per_xcd, (x+1) per_xcd), so the tiles that share an expert's weights
 // run side by side on one XCD's L2.  The grid, a multiple of 8 and at least
 // the largest possible tile count, covers every tile.
+//
+// Grouped tiles (xcd_local == 3; the grid a multiple of 8 kXcdGroup): the
+// logical tiles are cut into groups of kXcdGroup consecutive ids, one per
+// XCD and round, dealt round-robin (group 8 r + x to XCD x in round r).  One
+// round, 8 groups, is what the GPU runs at a time (one workgroup per CU), so
+// every XCD works on the same expert as the others (whose bytes the
+// memory-side cache then serves to all of them), and each XCD's own group is
+// a compact block of tiles (with n_group 4: 8 m-tiles x 4 n-tiles), whose
+// 8 row blocks and 4 weight panels its L2 serves to its 32 CUs.  Plain
+// round-robin order gives each XCD 32 row blocks and one panel per round.
+// The last round, when partial, is dealt round-robin tile by tile, so that
+// every XCD takes a share of it.
+constexpr int kXcdGroup = 32;  // workgroups one XCD runs at a time: one per CU
+
 template <bool DENSE = false, class G>
 __device__ __forceinline__ int block_tile(const G& g) {
   int total;
   if constexpr (DENSE) total = g.dense_total;
   else total = g.tile_base[g.e_loc] * g.n_tiles;
+  if (g.xcd_local == 3) {
+    const int x = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int base = slot / kXcdGroup * (8 * kXcdGroup), j = slot % kXcdGroup;
+    const int L = base + 8 * kXcdGroup <= total ? base + x * kXcdGroup + j : base + 8 * j + x;
+    return L < total ? L : -1;
+  }
   if (g.xcd_local != 1) return (int)blockIdx.x < total ? (int)blockIdx.x : -1;
   const int per_xcd = (total + 7) >> 3;
   const int slot = blockIdx.x >> 3;

@@ -306,6 +306,33 @@ def check_ep_shares_sum(O, seed=8):
         assert np.allclose(full[t], ref, rtol=1e-10, atol=1e-10)
 
 
+def check_permute_slots(O, seed=9):
+    """Permute against its definition from the slot side: every resident
+    (token, slot) pair owns one row, whose x_perm row is that token's hidden
+    row, and no row is left over (each (token, slot) appears exactly once)."""
+    rng = np.random.default_rng(seed)
+    for (T, k, E, E_loc, e0) in [(1, 1, 3, 3, 0), (29, 3, 10, 10, 0), (64, 4, 16, 6, 5), (40, 8, 64, 32, 32)]:
+        logits = rng.standard_normal((T, E)).astype(np.float32)
+        x = rng.standard_normal((T, 5)).astype(np.float32)
+        idx, _ = O.route(logits, k)
+        le = O.local_map(idx, e0, E_loc)
+        counts, offsets, ros, tor = O.layout(le, E_loc)
+        xp = O.permute(x, tor)
+        R = int(offsets[-1])
+        assert xp.shape == (R, 5)
+        seen = np.zeros(R, np.int64)
+        for t in range(T):
+            for j in range(k):
+                r = int(ros[t, j])
+                if le[t, j] < 0:
+                    assert r == -1
+                    continue
+                seen[r] += 1
+                for h in range(5):
+                    assert xp[r, h] == x[t, h], (T, t, j, r)
+        assert np.all(seen == 1)
+
+
 ALL_CHECKS = [
     check_router_bruteforce,
     check_router_one_hot,
@@ -319,5 +346,6 @@ ALL_CHECKS = [
     check_ffn_bruteforce,
     check_dense_mlp,
     check_identity_experts,
+    check_permute_slots,
     check_ep_shares_sum,
 ]

@@ -141,6 +141,16 @@ def _ffn_sign(xp, offsets, w_gu, w_dn):
     return h, _down(h, offsets, w_dn)
 
 
+def _permute_by_row(x, token_of_row):
+    # gathers row r from x[r] instead of x[token_of_row[r]]
+    R = len(token_of_row)
+    return x[np.arange(R) % max(len(x), 1)] if len(x) else x[:0]
+
+
+def _permute_next_token(x, token_of_row):
+    return x[np.minimum(np.asarray(token_of_row, np.int64) + 1, len(x) - 1)]
+
+
 def _combine_unweighted(y, w, ros, T, H):
     return M.combine(y, np.ones_like(w), ros, T, H)
 
@@ -183,6 +193,8 @@ MUTANTS = {
     "ffn_missing_up_term": dict(expert_ffn=_ffn_no_up_fixed),
     "ffn_down_reshaped_not_transposed": dict(expert_ffn=_ffn_reshape_down),
     "ffn_silu_sign": dict(expert_ffn=_ffn_sign),
+    "permute_gathers_by_row_index": dict(permute=_permute_by_row),
+    "permute_next_token": dict(permute=_permute_next_token),
     "combine_unweighted": dict(combine=_combine_unweighted),
     "combine_first_weight_only": dict(combine=_combine_first_weight),
     "combine_drops_last_slot": dict(combine=_combine_drop_last),

@@ -286,6 +286,34 @@ int moe_combine(moe_ctx_t* ctx, int phase, void* out, hipStream_t stream);
  * Errors: MOE_ERR_INVALID_ARG (null), MOE_ERR_INVALID_PHASE. */
 int moe_phase_view(const moe_ctx_t* ctx, int phase, moe_phase_view_t* view);
 
+/* Allocation-free dispatch layout, for callers that cannot allocate device
+ * memory: code under graph capture, tight serving loops, harnesses that
+ * forbid allocation.  It runs the kernels of moe_dispatch_layout on caller
+ * buffers, with no context: from the routing indices it writes
+ *   counts [E_loc], offsets [E_loc + 1], row_of_slot [T, k] (-1 = dropped)
+ *   and token_of_row [R], R = offsets[E_loc] <= T * min(k, E_loc),
+ * the same layout moe_dispatch_layout gives (rows of an expert in ascending
+ * token order, no padding).
+ * topk_idx: borrowed device [T, k] int32 global expert ids (as moe_route
+ * writes them); expert_begin / num_local_experts: the resident block
+ * [e0, e0 + E_loc).  All pointers are device pointers the caller owns, valid
+ * until the work completes on `stream`; token_of_row must have room for
+ * T * min(k, E_loc) entries.  T = 0 is legal (counts and offsets are zeroed).
+ * It allocates nothing: the kernels' scratch (histogram cells and the m-tile
+ * prefix, 33,796 bytes) is a fixed device array that each device holds until
+ * the process ends, looked up on the first call on a device.  Every call on
+ * a device shares that array, so calls that overlap on one device (other
+ * streams or host threads) race and must be serialised by the caller.
+ * Limits: T <= MOE_NOALLOC_MAX_TOKENS, 1 <= k <= 16, 1 <= E_loc <= 256.
+ * Errors: MOE_ERR_INVALID_ARG (null pointer where T > 0 needs one, null
+ * counts/offsets/stream, T < 0, k or E_loc out of range, e0 < 0),
+ * MOE_ERR_CAPACITY (T above the limit), MOE_ERR_HIP.  A call refused for its
+ * arguments enqueues nothing. */
+#define MOE_NOALLOC_MAX_TOKENS (1 << 20)
+int moe_dispatch_layout_noalloc(const int32_t* topk_idx, int32_t T, int32_t top_k, int32_t expert_begin,
+                                int32_t num_local_experts, int32_t* counts, int32_t* offsets, int32_t* row_of_slot,
+                                int32_t* token_of_row, hipStream_t stream);
+
 /* Explicit transition back to IDLE (cancellation).  Succeeds only when every
  * operation enqueued for the phase has completed on the GPU; otherwise returns
  * MOE_ERR_BUSY and changes nothing.  Never touches the other phase.

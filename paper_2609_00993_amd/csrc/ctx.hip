@@ -94,20 +94,6 @@ bool valid_config(const moe_config_t* c) {
   return true;
 }
 
-// Chunking of the dispatch histogram for T tokens: one chunk up to
-// kOneChunkSlots slots, else about 256 slots per chunk, and never more than
-// kMaxCells (expert, chunk) cells.
-void chunking(int T, int k, int e_loc, int* tc_out, int* nchunks_out) {
-  int tc = dispatch_chunk_tokens(T, k, e_loc);
-  int nc = T > 0 ? (T + tc - 1) / tc : 1;
-  while ((long long)nc * e_loc > kMaxCells) {
-    ++tc;
-    nc = (T + tc - 1) / tc;
-  }
-  *tc_out = tc;
-  *nchunks_out = nc < 1 ? 1 : nc;
-}
-
 int max_chunks(int e_loc) { return kMaxCells / e_loc; }
 
 void free_timing(Phase& p) {
@@ -274,7 +260,7 @@ MxBuffers mx_of(const moe_ctx* ctx, const Phase& p) {
 int layout(moe_ctx* ctx, Phase& p, hipStream_t stream) {
   const moe_config_t& c = ctx->cfg;
   const int T = p.T, k = c.top_k, E_loc = c.num_local_experts;
-  chunking(T, k, E_loc, &p.chunk_tokens, &p.nchunks);
+  dispatch_chunking(T, k, E_loc, &p.chunk_tokens, &p.nchunks);
   if (c.dtype == MOE_DTYPE_FP8) {
     const long long avg = (long long)T * k / c.num_experts;
     p.regime = avg >= 32 ? 0 : 1;

@@ -67,6 +67,20 @@ inline int dispatch_chunk_tokens(int T, int k, int e_loc) {
   return tc < 1 ? 1 : tc;
 }
 
+// Chunking of the dispatch histogram for T tokens: one chunk up to
+// kOneChunkSlots slots, else about 256 slots per chunk, and never more than
+// kMaxCells (expert, chunk) cells.
+inline void dispatch_chunking(int T, int k, int e_loc, int* tc_out, int* nchunks_out) {
+  int tc = dispatch_chunk_tokens(T, k, e_loc);
+  int nc = T > 0 ? (T + tc - 1) / tc : 1;
+  while ((long long)nc * e_loc > kMaxCells) {
+    ++tc;
+    nc = (T + tc - 1) / tc;
+  }
+  *tc_out = tc;
+  *nchunks_out = nc < 1 ? 1 : nc;
+}
+
 // How the route kernel forms its logits after the router GEMM (out == null:
 // read them as given).  logit[t][e] = sum over s < nsplit of
 // in[(s T + t) E + e], in split order, + bias[e] (bias may be null); stored

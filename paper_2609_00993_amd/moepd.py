@@ -133,6 +133,8 @@ _SIGNATURES = {
     "moe_dispatch": (c_int, [c_void_p, c_int, c_void_p, c_void_p]),
     "moe_dispatch_layout": (c_int, [c_void_p, c_int, c_void_p]),
     "moe_dispatch_permute": (c_int, [c_void_p, c_int, c_void_p, c_void_p]),
+    "moe_dispatch_layout_noalloc": (c_int, [c_void_p, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
+                                            c_void_p, c_void_p, c_void_p]),
     "moe_expert_ffn": (c_int, [c_void_p, c_int, c_void_p]),
     "moe_combine": (c_int, [c_void_p, c_int, c_void_p, c_void_p]),
     "moe_phase_view": (c_int, [c_void_p, c_int, POINTER(moe_phase_view_t)]),
@@ -250,6 +252,12 @@ def moe_dispatch(ctx, phase: int, x, stream) -> int:
 
 def moe_dispatch_layout(ctx, phase: int, stream) -> int:
     return _lib.moe_dispatch_layout(ctx, phase, _stream(stream))
+
+
+def moe_dispatch_layout_noalloc(topk_idx, T: int, top_k: int, expert_begin: int, num_local_experts: int, counts,
+                                offsets, row_of_slot, token_of_row, stream) -> int:
+    return _lib.moe_dispatch_layout_noalloc(_ptr(topk_idx), T, top_k, expert_begin, num_local_experts, _ptr(counts),
+                                            _ptr(offsets), _ptr(row_of_slot), _ptr(token_of_row), _stream(stream))
 
 
 def moe_dispatch_permute(ctx, phase: int, x, stream) -> int:

@@ -134,3 +134,28 @@ def test_clock_probe_rejects_bad_arguments(lib):
     assert M.moe_clock_probe(16, 100, None) == M.MOE_ERR_INVALID_ARG  # null output
     assert M.moe_clock_probe(16, 0, 16) == M.MOE_ERR_INVALID_ARG
     assert M.moe_clock_probe(16, 100001, 16) == M.MOE_ERR_INVALID_ARG
+
+
+def test_noalloc_layout_validates_on_the_host(lib):
+    """The allocation-free layout refuses bad arguments before any HIP call
+    (fake pointers, no GPU needed)."""
+    fake = 0x1000
+
+    def call(**kw):
+        a = dict(topk_idx=fake, T=4, top_k=2, expert_begin=0, num_local_experts=8, counts=fake, offsets=fake,
+                 row_of_slot=fake, token_of_row=fake, stream=fake)
+        a.update(kw)
+        return lib.moe_dispatch_layout_noalloc(**a)
+
+    assert call(T=-1) == lib.MOE_ERR_INVALID_ARG
+    assert call(top_k=0) == lib.MOE_ERR_INVALID_ARG
+    assert call(top_k=17) == lib.MOE_ERR_INVALID_ARG
+    assert call(expert_begin=-1) == lib.MOE_ERR_INVALID_ARG
+    assert call(num_local_experts=0) == lib.MOE_ERR_INVALID_ARG
+    assert call(num_local_experts=257) == lib.MOE_ERR_INVALID_ARG
+    assert call(counts=None) == lib.MOE_ERR_INVALID_ARG
+    assert call(offsets=None) == lib.MOE_ERR_INVALID_ARG
+    assert call(stream=None) == lib.MOE_ERR_INVALID_ARG
+    assert call(topk_idx=None) == lib.MOE_ERR_INVALID_ARG
+    assert call(row_of_slot=None) == lib.MOE_ERR_INVALID_ARG
+    assert call(T=(1 << 20) + 1) == lib.MOE_ERR_CAPACITY

@@ -106,8 +106,9 @@ __device__ __forceinline__ void gemm_skinny_tile(const GemmArgs& g, const TileCo
   // l: row 8i + l/8, 16-byte chunk l%8): reading 16 bytes from each of 32
   // rows per instruction, as the MFMA lane layout would, reaches only about a
   // quarter of the per-CU rate of whole-line reads.  The block then goes
-  // through this wave's LDS stage, chunk c of row r at slot 8r + (c ^ r%8)
-  // (no bank conflicts on either side), and is read back in the MFMA layout.
+  // through this wave's LDS stage, chunk c of row r at slot
+  // 8r + (c ^ stage_swz(r)) (no bank conflicts on either side), and is read
+  // back in the MFMA layout.
   __shared__ u32x4 stage[NP][32 * 8];
   const int lane = threadIdx.x & 63;
   const int lr = lane >> 3, lc = lane & 7;  // coalesced side: row within eight, chunk
@@ -132,12 +133,14 @@ __device__ __forceinline__ void gemm_skinny_tile(const GemmArgs& g, const TileCo
 #pragma unroll
     for (int j = 0; j < NB; ++j) off[1 + j][i] = cc;
   }
-  const int wslot = lr * 8 + (lc ^ lr);
+  int wslot[4];  // LDS slot of this lane's chunk for each of the four instructions
+#pragma unroll
+  for (int i = 0; i < 4; ++i) wslot[i] = (8 * i + lr) * 8 + (lc ^ stage_swz(8 * i + lr));
   // lane group kg holds k in [64*kb + 32*kg, +32) as four 16-byte chunks;
   // MFMA step s takes chunk s of both groups (the same k map for A and B).
   int rslot[4];
 #pragma unroll
-  for (int st = 0; st < 4; ++st) rslot[st] = r * 8 + ((4 * kg + st) ^ (r & 7));
+  for (int st = 0; st < 4; ++st) rslot[st] = r * 8 + ((4 * kg + st) ^ stage_swz(r));
 
   f32x16_t acc[NB];
 #pragma unroll
@@ -172,7 +175,7 @@ __device__ __forceinline__ void gemm_skinny_tile(const GemmArgs& g, const TileCo
 #pragma unroll
         for (int p = 0; p < NP; ++p)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) stage[p][64 * i + wslot] = v[q][p][i];
+          for (int i = 0; i < 4; ++i) stage[p][wslot[i]] = v[q][p][i];
         if (kb + PF < KB) load(kb + PF, v[q]);
 #pragma unroll
         for (int st = 0; st < 4; ++st) {

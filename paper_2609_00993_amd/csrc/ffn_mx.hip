@@ -163,7 +163,7 @@ constexpr int kMxDecodeWaves = 1;
 // A 128-deep K block of a panel (the tile's 32 code rows, or its 32 gate or
 // up weight rows) is 4 KB: it is loaded by four 1 KB whole-line reads (lane
 // l: row 8i + l/8, 16-byte unit l%8), written to this wave's LDS stage (unit
-// c of row r at slot 8r + (c ^ r%8), no bank conflicts either way) and read
+// c of row r at slot 8r + (c ^ stage_swz(r)), no bank conflicts either way) and read
 // back in the MFMA lane layout; reading 16 bytes from each of 32 rows per
 // instruction reaches only about a quarter of the per-CU rate of whole-line
 // reads.  A row's four scale bytes of the block come as one 4-byte load.
@@ -210,14 +210,16 @@ __device__ __forceinline__ void gemm_mx_skinny_tile(const GemmArgsMX& g, const T
   soff[0] = min(tc.m0 + r, tc.m_end - 1) * kw;
 #pragma unroll
   for (int j = 0; j < NB; ++j) soff[1 + j] = (col0 + r) * kw;
-  const int wslot = lr * 8 + (lc ^ lr);
+  int wslot[4];  // LDS slot of this lane's chunk for each of the four instructions
+#pragma unroll
+  for (int i = 0; i < 4; ++i) wslot[i] = (8 * i + lr) * 8 + (lc ^ stage_swz(8 * i + lr));
   // Step s (64 deep) of a block: lane (r, h) holds units 4s + h and 4s + 2 + h
   // of its row and the scale of 32-value block 2s + h.
   int rslot[2][2];
 #pragma unroll
   for (int st = 0; st < 2; ++st)
 #pragma unroll
-    for (int u = 0; u < 2; ++u) rslot[st][u] = r * 8 + ((4 * st + 2 * u + h) ^ (r & 7));
+    for (int u = 0; u < 2; ++u) rslot[st][u] = r * 8 + ((4 * st + 2 * u + h) ^ stage_swz(r));
 
   f32x16_mx acc[NB];
 #pragma unroll
@@ -246,7 +248,7 @@ __device__ __forceinline__ void gemm_mx_skinny_tile(const GemmArgsMX& g, const T
 #pragma unroll
     for (int p = 0; p < NP; ++p)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) stage[p][64 * i + wslot] = d[p][i];
+      for (int i = 0; i < 4; ++i) stage[p][wslot[i]] = d[p][i];
   };
   // Scale words of the block pair in flight (SC2) or of each block.
   typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));

@@ -50,6 +50,15 @@ __device__ __forceinline__ int swz(int row) {
   return (row / RPS) & (CPR - 1);
 }
 
+// Swizzle of the small-batch tiles' per-wave LDS stage: a 64-deep K block of
+// 32 rows, chunk c (16 bytes) of row r at slot 8 r + (c ^ stage_swz(r)).  A
+// 16-lane group of the whole-line writes covers two rows, which share the
+// swizzle, so it writes 256 consecutive bytes; a 16-lane group of the MFMA
+// reads takes one chunk of 16 consecutive rows, whose slots then fall on
+// (r % 2, stage_swz(r)) = 16 different 16-byte bank groups.  (Swizzling by
+// r % 8 put rows r and r + 8 on the same banks: two-way conflicts.)
+__device__ __forceinline__ int stage_swz(int row) { return (row >> 1) & 7; }
+
 // Workgroup barrier without a memory fence; the signal fences keep the
 // compiler from moving LDS accesses across it.  Visibility of the DMA'd
 // stages is established by wait_vmcnt before the barrier.

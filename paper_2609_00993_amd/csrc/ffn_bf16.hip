@@ -346,7 +346,16 @@ __device__ __forceinline__ int read_window_cell(const void* cell) {
 }
 constexpr int kCachePolicyAgent = 0x10;  // sc1: coherent at agent scope
 
-template <int BM, int BR, int BK, int WM, int WN, bool GATED, int STAGES, bool DENSE = false>
+// STAGES slots hold weight slices; SA >= STAGES slots hold activation
+// slices.  With SA = STAGES + 1 (two weight slots only) the activation
+// slices are issued one slice further ahead than the weight slices: slice j's
+// DMA group is [B(j), A(j + 1)], so the counted wait at a slice end retires
+// the next slice's weights while that slice's activations, issued a slice
+// earlier, have had two slices' time to land.  WIN: the tile keeps the LDS
+// cells of the D window word (tiles that never yield leave them out, which
+// frees the LDS for the third activation slot).
+template <int BM, int BR, int BK, int WM, int WN, bool GATED, int STAGES, bool DENSE = false, int SA = STAGES,
+          bool WIN = true>
 __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   constexpr int NB = GATED ? 2 : 1;
   constexpr int BN = BR / NB;
@@ -365,14 +374,20 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   static_assert(A_INS * RPI * 4 == BM && B_INS * RPI * 4 == BR, "slices split into whole DMA instructions");
   static_assert(FM * 32 == WTM && FN * 32 == WTN, "wave tile must be a multiple of 32x32");
   static_assert(STAGES >= 2 && NPS * (STAGES - 1) < 64, "pipeline depth");
-  // One LDS object: the ring of K slices, then the cells of the D window
-  // word (its first word in each cell, see load_window).
-  struct Lds {
-    u32x4 ring[STAGES][A_CH + B_CH];
+  constexpr int LEAD = SA - STAGES;  // slices the activations run ahead of the weights
+  static_assert(LEAD == 0 || (LEAD == 1 && STAGES == 2 && !WIN && !DENSE), "activation lead: two weight slots only");
+  static_assert(2 * A_INS + B_INS < 64, "prologue wait range");
+  // One LDS object: the activation and weight rings of K slices, then (WIN)
+  // the cells of the D window word (its first word in each cell, see
+  // load_window).
+  struct LdsRings {
+    u32x4 a[SA][A_CH];
+    u32x4 b[STAGES][B_CH];
+  };
+  struct LdsWin : LdsRings {
     u32x4 window[64];
   };
-  __shared__ Lds lds;
-  auto& ring = lds.ring;
+  __shared__ std::conditional_t<WIN, LdsWin, LdsRings> lds;
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -413,33 +428,50 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
       b_src[i] = Be + (size_t)brow * g.K + k0 + (lphys ^ swz<BK>(r)) * 8;
     }
   };
-  auto issue = [&](int kt, int slot) {
+  auto issue_a = [&](int kt, int slot) {
     const int koff = kt * BK;
 #pragma unroll
     for (int i = 0; i < A_INS; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, MOEPD_LPTR(&ring[slot][(wave * A_INS + i) * 64]), 16,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, MOEPD_LPTR(&lds.a[slot][(wave * A_INS + i) * 64]), 16,
                                                a_off[i] + (uint32_t)koff * 2u, 0, 0, 0);
+  };
+  auto issue_b = [&](int kt, int slot) {
+    const int koff = kt * BK;
 #pragma unroll
     for (int i = 0; i < B_INS; ++i)
-      __builtin_amdgcn_global_load_lds(MOEPD_GPTR(b_src[i] + koff),
-                                       MOEPD_LPTR(&ring[slot][A_CH + (wave * B_INS + i) * 64]), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(MOEPD_GPTR(b_src[i] + koff), MOEPD_LPTR(&lds.b[slot][(wave * B_INS + i) * 64]),
+                                       16, 0, 0);
+  };
+  // DMA group of slice j: without a lead, A(j) then B(j) into slot j % STAGES;
+  // with the activation lead, B(j) into weight slot j % 2, then A(j + 1) (if
+  // the tile has it) into activation slot (j + 1) % 3.
+  auto issue = [&](int kt, int bslot, int aslot_next) {
+    if constexpr (LEAD == 0) {
+      issue_a(kt, bslot);
+      issue_b(kt, bslot);
+    } else {
+      issue_b(kt, bslot);
+      if (kt + 1 < KT) issue_a(kt + 1, aslot_next);
+    }
   };
   auto load_window = [&] {
-    __builtin_amdgcn_global_load_lds(MOEPD_GPTR(g.yield.word), MOEPD_LPTR(&lds.window[0]), 16, 0,
-                                     kCachePolicyAgent);
+    if constexpr (WIN)
+      __builtin_amdgcn_global_load_lds(MOEPD_GPTR(g.yield.word), MOEPD_LPTR(&lds.window[0]), 16, 0,
+                                       kCachePolicyAgent);
   };
   auto prologue = [&](const TileCoord& tc) {
     set_sources(tc);
+    if constexpr (LEAD == 1) issue_a(0, 0);
 #pragma unroll
     for (int st = 0; st < STAGES; ++st)
-      if (st < KT) issue(st, st);
-    if (g.yield.word) load_window();
+      if (st < KT) issue(st, st, st + 1);
+    if (WIN && g.yield.word) load_window();
   };
 
   bf16x8_t fa[2][FM], fb[2][FB];
-  auto read_frags = [&](int slot, int sub, bf16x8_t (&a)[FM], bf16x8_t (&b)[FB]) {
-    const u32x4* As = &ring[slot][0];
-    const u32x4* Bs = &ring[slot][A_CH];
+  auto read_frags = [&](int aslot, int bslot, int sub, bf16x8_t (&a)[FM], bf16x8_t (&b)[FB]) {
+    const u32x4* As = &lds.a[aslot][0];
+    const u32x4* Bs = &lds.b[bslot][0];
     const int ch = 2 * sub + (lane >> 5);
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm) {
@@ -487,36 +519,53 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // slice 0 has landed once at most min(STAGES - 1, KT - 1) newer slices remain
-  wait_slices_lgkm0<NPS, STAGES - 1>(min(STAGES - 1, KT - 1));
+  // Slice 0 has landed once at most min(STAGES - 1, KT - 1) newer slices
+  // remain; with the activation lead, once at most A(1), B(1) and A(2) (those
+  // the tile has) remain behind B(0).
+  if constexpr (LEAD == 0) {
+    wait_slices_lgkm0<NPS, STAGES - 1>(min(STAGES - 1, KT - 1));
+  } else {
+    if (KT > 2) wait_vmcnt_lgkm0<2 * A_INS + B_INS>();
+    else if (KT == 2) wait_vmcnt_lgkm0<A_INS + B_INS>();
+    else wait_vmcnt_lgkm0<0>();
+  }
   bare_barrier();
-  read_frags(0, 0, fa[0], fb[0]);
+  read_frags(0, 0, 0, fa[0], fb[0]);
 
   // One K slice.  MODE 0: slice kt + STAGES is issued into this slot after
   // the barrier; MODE 1: no slices left to issue; MODE 2: the tile's last
   // slice (no barrier, nothing to read ahead).  The three loops below keep
   // each body straight-line code, so the accumulators stay in place.
-  auto slice = [&](auto mode, int kt, int slot) {
+  auto slice = [&](auto mode, int kt, int aslot, int bslot) {
     constexpr int MODE = decltype(mode)::value;
 #pragma unroll
     for (int sub = 0; sub < SUB; ++sub) {
       const int cur = sub & 1, nxt = cur ^ 1;
       if (sub + 1 < SUB) {
-        read_frags(slot, sub + 1, fa[nxt], fb[nxt]);
+        read_frags(aslot, bslot, sub + 1, fa[nxt], fb[nxt]);
         mfmas(fa[cur], fb[cur]);
         interleave<0, NMF, 0, NRD, 0>();
       } else if constexpr (MODE < 2) {
-        // Every read of this slot is in registers once lgkmcnt is 0; slice
+        // Every read of this slot is in registers once lgkmcnt is 0.  Slice
         // kt + 1 has landed once at most min(STAGES - 2, KT - 2 - kt) newer
-        // slices remain.  After the barrier no wave reads this slot again,
-        // so slice kt + STAGES may overwrite it.
-        if constexpr (MODE == 0) wait_vmcnt_lgkm0<NPS * (STAGES - 2)>();
-        else wait_slices_lgkm0<NPS, STAGES - 2>(min(STAGES - 2, KT - 2 - kt));
+        // slices remain; with the activation lead, once at most A(kt + 2)
+        // (if the tile has it) remains behind B(kt + 1), A(kt + 1) having been
+        // issued a group earlier.  After the barrier no wave reads this slot
+        // again, so slice kt + STAGES (and A(kt + 3)) may overwrite it.
+        if constexpr (LEAD == 1) {
+          if (kt + 2 < KT) wait_vmcnt_lgkm0<A_INS>();
+          else wait_vmcnt_lgkm0<0>();
+        } else if constexpr (MODE == 0) {
+          wait_vmcnt_lgkm0<NPS * (STAGES - 2)>();
+        } else {
+          wait_slices_lgkm0<NPS, STAGES - 2>(min(STAGES - 2, KT - 2 - kt));
+        }
         bare_barrier();
-        int ns = slot + 1;
-        if (ns == STAGES) ns = 0;
+        int nb = bslot + 1, na = aslot + 1;
+        if (nb == STAGES) nb = 0;
+        if (na == SA) na = 0;
         if constexpr (MODE == 0) {
-          issue(kt + STAGES, slot);
+          issue(kt + STAGES, bslot, aslot);
           // D first inside a tile: every kPauseEvery slices, a P tile that
           // found the D window open at the previous check (or at the tile's
           // start) pauses until it closes (within the tile's wait budget), so
@@ -524,13 +573,15 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
           // bandwidth.  The word read here was loaded into LDS one check
           // ahead, so its load never stalls the pipeline; its LDS read
           // completes before the next load into the same words is issued.
-          if (g.yield.word && (kt & (kPauseEvery - 1)) == kPauseEvery - 1) {
-            const int seen = __builtin_amdgcn_readfirstlane(read_window_cell(&lds.window[lane]));
-            if (seen == g.yield.gen) yield_to_window(g.yield, wait_budget);
-            load_window();
+          if constexpr (WIN) {
+            if (g.yield.word && (kt & (kPauseEvery - 1)) == kPauseEvery - 1) {
+              const int seen = __builtin_amdgcn_readfirstlane(read_window_cell(&lds.window[lane]));
+              if (seen == g.yield.gen) yield_to_window(g.yield, wait_budget);
+              load_window();
+            }
           }
         }
-        read_frags(ns, 0, fa[nxt], fb[nxt]);
+        read_frags(na, nb, 0, fa[nxt], fb[nxt]);
         mfmas(fa[cur], fb[cur]);
         interleave<0, NMF, MODE == 0 ? NPS : 0, NRD, 1>();
       } else {
@@ -538,16 +589,20 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
       }
     }
   };
-  int kt = 0, slot = 0;
+  int kt = 0, aslot = 0, bslot = 0;
+  auto advance = [&] {
+    if (++bslot == STAGES) bslot = 0;
+    if (++aslot == SA) aslot = 0;
+  };
   for (; kt < KT - STAGES; ++kt) {
-    slice(std::integral_constant<int, 0>{}, kt, slot);
-    if (++slot == STAGES) slot = 0;
+    slice(std::integral_constant<int, 0>{}, kt, aslot, bslot);
+    advance();
   }
   for (; kt < KT - 1; ++kt) {
-    slice(std::integral_constant<int, 1>{}, kt, slot);
-    if (++slot == STAGES) slot = 0;
+    slice(std::integral_constant<int, 1>{}, kt, aslot, bslot);
+    advance();
   }
-  slice(std::integral_constant<int, 2>{}, kt, slot);
+  slice(std::integral_constant<int, 2>{}, kt, aslot, bslot);
 
   // epilogue: SwiGLU -> bf16 h (four columns = one 8-byte store), or
   // float32 y (four columns = one 16-byte store).  A lane's row is fixed,
@@ -601,11 +656,19 @@ __global__ __launch_bounds__(256) void gemm2_down_prefill(GemmArgs g) { gemm_rin
 // The router GEMM: logits = x Wr^T over all T rows, 64 x 128 tiles, K split
 // so that small batches still spread over the GPU.
 __global__ __launch_bounds__(256) void router_gemm(GemmArgs g) { gemm_ring_body<64, 128, 64, 2, 2, false, 3, true>(g); }
-// GEMM1's wide tiles take 64-deep slices in two stages (4 % faster than 32-deep
-// slices in four at the 16384-token skewed batch); GEMM2 measured the same
-// either way and keeps the four-stage ring.
-__global__ __launch_bounds__(256) void gemm1_swiglu_wide(GemmArgs g) { gemm_ring_body<256, 256, 64, 2, 2, true, 2>(g); }
-__global__ __launch_bounds__(256) void gemm2_down_wide(GemmArgs g) { gemm_ring_body<256, 256, 32, 2, 2, false, 4>(g); }
+// The wide tiles never yield (a P workgroup waiting on its CU would only keep
+// D off it), so they leave out the window cells.  GEMM1's take 64-deep
+// slices, two weight slots and three activation slots, the activations one
+// slice ahead (160 KB; at the 16384-token skewed batch 4 % faster than
+// 32-deep slices in four stages, and the third activation slot 1.4 % faster
+// than a two-slot ring); GEMM2 measured the same either way and keeps the
+// four-stage ring of 32-deep slices.
+__global__ __launch_bounds__(256) void gemm1_swiglu_wide(GemmArgs g) {
+  gemm_ring_body<256, 256, 64, 2, 2, true, 2, false, 3, false>(g);
+}
+__global__ __launch_bounds__(256) void gemm2_down_wide(GemmArgs g) {
+  gemm_ring_body<256, 256, 32, 2, 2, false, 4, false, 4, false>(g);
+}
 template <bool ROT, bool STAGE>
 __global__ __launch_bounds__(64 * kDecodeWaves) void gemm1_swiglu_decode(GemmArgs g) {
   gemm_skinny<true, ROT, STAGE>(g);
@@ -662,7 +725,6 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
     if (regime == 0) {
       if (gemm == 1) gemm1_swiglu_prefill<<<grid, 256, 0, s>>>(g);
       else gemm2_down_prefill<<<grid, 256, 0, s>>>(g);
-
     } else {
       if (gemm == 1) gemm1_swiglu_wide<<<grid, 256, 0, s>>>(g);
       else gemm2_down_wide<<<grid, 256, 0, s>>>(g);

@@ -57,6 +57,12 @@ SPECS = {
     # P, with ragged expert tails, a partial gate/up n-tile and dropped slots
     "wide-bf16": lambda: make_layer(LayerSpec("wide-bf16", E=8, e0=2, E_loc=4, k=2, H=256, I=192, dtype=BF16,
                                               T_P=2500, T_D=5), seed=15),
+    # the 256-row tiles over one and two 64-deep K slices: the shortest
+    # pipelines of GEMM1's ring, whose activation slices run one ahead
+    "wide-k64-bf16": lambda: make_layer(LayerSpec("wide-k64-bf16", E=4, e0=0, E_loc=4, k=1, H=64, I=128, dtype=BF16,
+                                                  T_P=2100, T_D=3), seed=16),
+    "wide-k128-bf16": lambda: make_layer(LayerSpec("wide-k128-bf16", E=4, e0=0, E_loc=4, k=1, H=128, I=192,
+                                                   dtype=BF16, T_P=2100, T_D=3), seed=17),
     # k = E: every expert takes every token
     "k-eq-E-bf16": lambda: make_layer(LayerSpec("kE-bf16", E=4, e0=0, E_loc=4, k=4, H=64, I=64, dtype=BF16, T_P=129,
                                                 T_D=1), seed=14),

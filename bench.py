@@ -77,6 +77,9 @@ def parse():
     ap.add_argument("--no-router", action="store_true", help="skip the router-GEMM timing")
     ap.add_argument("--d-priority-us", type=int, default=500,
                     help="D-first admission: longest wait of a P GEMM tile for an in-flight D layer (0 = off)")
+    ap.add_argument("--solo", choices=("P", "D"), default=None,
+                    help="instead of the concurrent bench, run only this phase's layer back to back and report its "
+                         "per-kernel durations (for kernel profiles; prints a line of its own, not the headline)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="instead of the layer, time a plain device copy of this many MiB (the reference kernel "
                          "for scaling the HBM byte counters)")
@@ -97,20 +100,23 @@ def workload_name(spec):
             f"SwiGLU {spec.dtype}{skew}, P {spec.T_P} + D {spec.T_D} tokens concurrent on two streams")
 
 
-def kernel_units(spec, kernel, T, R, touched, esz, osz=None):
+def kernel_units(spec, kernel, T, R, touched, esz, osz=None, t_res=None):
     """(algorithmic bytes, algorithmic flops) of one launch of `kernel` for a
-    phase batch of T tokens with R resident rows over `touched` experts.
-    esz: bytes of an x element; osz: bytes per element of the GEMM operands
-    (weights, x_perm, h), scales included (1 + 1/32 for MX FP8)."""
+    phase batch of T tokens with R resident rows over `touched` experts, t_res
+    of the tokens having a resident slot.  esz: bytes of an x element; osz:
+    bytes per element of the GEMM operands (weights, x_perm, h), scales
+    included (1 + 1/32 for MX FP8)."""
     H, I, E, k = spec.H, spec.I, spec.E, spec.k
     osz = esz if osz is None else osz
+    t_res = T if t_res is None else t_res
     if kernel == "route":
         return T * E * 4 + T * k * 8, 0
     if kernel in ("count", "place"):
         return T * k * 4 * (1 if kernel == "count" else 2) + R * 4, 0
     if kernel == "permute":
-        tokens_touched = T  # every token row is read once (tokens with no resident slot too)
-        return int(tokens_touched * H * esz + R * H * osz), 0
+        # the rows of the tokens with a resident slot are read once (the
+        # others are skipped), each resident row written once
+        return int(t_res * H * esz + R * H * osz), 0
     if kernel == "gemm1_swiglu":
         return int(touched * 2 * I * H * osz + R * H * osz + R * I * osz), 4 * R * H * I
     if kernel == "gemm2_down":
@@ -328,10 +334,6 @@ def run_trace(args, M, inp, dev):
 
     # per-kernel events (D-first admission off), with each step's rows and
     # touched experts read back for the algorithmic units
-    import ctypes
-
-    hip = ctypes.CDLL("libamdhip64.so")
-    hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
     acc_units = {}
 
     def units(st, with_p):
@@ -339,12 +341,9 @@ def run_trace(args, M, inp, dev):
         for ph, T in ((0, st.t_p), (1, st.t_d)):
             if T == 0 or (ph == 0 and not with_p):
                 continue
-            _, v = M.moe_phase_view(ctx_off, ph)
-            counts = torch.empty(spec.E_loc, dtype=torch.int32)
-            assert hip.hipMemcpy(counts.data_ptr(), v.counts, spec.E_loc * 4, 2) == 0
-            R, touched = int(counts.sum()), int((counts > 0).sum())
+            R, touched, t_res = layout_counts(M, ctx_off, ph, spec)
             for name in ("route", "count", "place", "permute", "gemm1_swiglu", "gemm2_down", "combine"):
-                by, fl = kernel_units(spec, name, T, R, touched, 2)
+                by, fl = kernel_units(spec, name, T, R, touched, 2, None, t_res)
                 b0, f0 = acc_units.get((ph, name), (0, 0))
                 acc_units[(ph, name)] = (b0 + by, f0 + fl)
 
@@ -593,6 +592,66 @@ def router_measure(M, c, xs, T, spec, inp, sP, sD, bf16, reps=20):
     return out
 
 
+def layout_counts(M, c, ph, spec):
+    """Routed rows, touched experts and tokens with a resident slot of the
+    phase's latest layout (read from the device once)."""
+    import ctypes
+
+    import torch
+
+    st, v = M.moe_phase_view(c, ph)
+    M.check(st)
+    counts = torch.empty(spec.E_loc, dtype=torch.int32)
+    ros = torch.empty((max(v.tokens, 1), spec.k), dtype=torch.int32)
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+    assert hip.hipMemcpy(counts.data_ptr(), v.counts, spec.E_loc * 4, 2) == 0
+    if v.tokens:
+        assert hip.hipMemcpy(ros.data_ptr(), v.row_of_slot, v.tokens * spec.k * 4, 2) == 0
+    t_res = int((ros[:v.tokens] >= 0).any(dim=1).sum()) if v.tokens else 0
+    return int(counts.sum()), int((counts > 0).sum()), t_res
+
+
+def solo_run(args, M, c, ph, layer, spec, T, esz, osz):
+    """One phase alone: `steps` layers back to back on its stream, timed as a
+    whole and then again with per-kernel HIP events."""
+    import torch
+
+    for _ in range(max(1, args.warmup)):
+        layer(ph, c)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        layer(ph, c)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    M.check(M.moe_timing_enable(c, args.steps), "moe_timing_enable")
+    for _ in range(args.steps):
+        layer(ph, c)
+    torch.cuda.synchronize()
+    R, touched, t_res = layout_counts(M, c, ph, spec)
+    kernels = {}
+    for kid in range(M.MOE_NUM_KERNELS):
+        st, ms, n = M.moe_timing_read(c, ph, kid)
+        M.check(st)
+        if not n:
+            continue
+        name = M.moe_kernel_name(kid)
+        by, fl = kernel_units(spec, name, T, R, touched, esz, osz, t_res)
+        us = ms / n * 1e3
+        kernels[name] = {"mean_us": round(us, 2), "launches": n,
+                         "GB/s": round(by / (us * 1e-6) / 1e9, 1) if by else None,
+                         "TFLOP/s": round(fl / (us * 1e-6) / 1e12, 1) if fl else None}
+    M.check(M.moe_timing_enable(c, 0))
+    print(json.dumps({"solo": args.solo, "workload": workload_name(spec), "tokens": T, "tokens_resident": t_res,
+                      "rows": R,
+                      "touched_experts": touched, "steps": args.steps, "warmup": args.warmup,
+                      "ms_per_layer": round(wall / args.steps * 1e3, 4),
+                      "tokens_per_s": round(T * args.steps / wall, 1), "kernels": kernels,
+                      "note": "one phase alone, D-first admission off; kernels: per-kernel HIP events on the phase's "
+                              "stream over a second pass, algorithmic bytes and flops per launch"}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -645,6 +704,15 @@ def main():
         M.check(st, "moe_ctx_create")
         return c
 
+    if args.solo:
+        sS = torch.cuda.Stream(device=dev)
+        c = make_ctx(0)
+        ph = 0 if args.solo == "P" else 1
+        solo_run(args, M, c, ph, lambda p, cc: M.layer(cc, p, lg[p], T[p], xs[p], outs[p], sS), spec, T[ph], esz,
+                 osz)
+        M.check(M.moe_ctx_destroy(c))
+        return
+
     # The bench line runs at the D-first admission bound given (ctx); the same
     # layer without it (ctx_off) gives the comparison figures and the
     # per-kernel durations, which must not include P's deliberate waits.
@@ -692,18 +760,9 @@ def main():
     M.check(M.moe_timing_enable(ctx_off, 0))
 
     # rows and touched experts of each phase (device-side layout, read once)
-    rows, touched = {}, {}
+    rows, touched, t_res = {}, {}, {}
     for ph in (0, 1):
-        st, v = M.moe_phase_view(ctx, ph)
-        M.check(st)
-        counts = torch.empty(spec.E_loc, dtype=torch.int32)
-        import ctypes
-
-        hip = ctypes.CDLL("libamdhip64.so")
-        hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
-        assert hip.hipMemcpy(counts.data_ptr(), v.counts, spec.E_loc * 4, 2) == 0
-        rows[ph] = int(counts.sum())
-        touched[ph] = int((counts > 0).sum())
+        rows[ph], touched[ph], t_res[ph] = layout_counts(M, ctx, ph, spec)
 
     # ---- D latency alone and under P
     # D alone is measured back to back (the layer's weights partly stay in the
@@ -821,7 +880,7 @@ def main():
     ph_d, name_d = dom
     ms_d, n_d = kern[dom]
     avg_s = ms_d / n_d / 1e3
-    by, fl = kernel_units(spec, name_d, T[ph_d], rows[ph_d], touched[ph_d], esz, osz)
+    by, fl = kernel_units(spec, name_d, T[ph_d], rows[ph_d], touched[ph_d], esz, osz, t_res[ph_d])
     t_hbm = by / (HBM_PEAK_GBS * 1e9)
     t_mfma = fl / (mma_peak * 1e12) if packed else fl / (FP32_VECTOR_PEAK_TFLOPS * 1e12)
     if fl and t_mfma >= t_hbm:
@@ -838,7 +897,7 @@ def main():
 
     kernels = {}
     for (ph, name), (ms, n) in sorted(kern.items()):
-        by_k, fl_k = kernel_units(spec, name, T[ph], rows[ph], touched[ph], esz, osz)
+        by_k, fl_k = kernel_units(spec, name, T[ph], rows[ph], touched[ph], esz, osz, t_res[ph])
         us = ms / n * 1e3
         kernels[f"{'P' if ph == 0 else 'D'}.{name}"] = {
             "mean_us": round(us, 2),

@@ -205,7 +205,10 @@ typedef struct moe_ctx moe_ctx_t;
 /* Create a context on the current HIP device.  Validates cfg (see field
  * comments), allocates both phases' buffers at capacity (disjoint
  * allocations, fixed for the context's lifetime) and their events.  Creates no
- * stream.  Errors: MOE_ERR_INVALID_ARG (null pointer, size out of range, k > E,
+ * stream.  Section 5.1 and its ownership table: the phases share the model
+ * weights (here the borrowed w) and nothing a kernel writes; each phase owns
+ * its buffers, counters, workspace and events, and D keeps stable addresses
+ * for its captured graphs.  Errors: MOE_ERR_INVALID_ARG (null pointer, size out of range, k > E,
  * e0 + E_loc > E, flags != 0), MOE_ERR_OOM, MOE_ERR_HIP.  On error *out is
  * NULL and nothing is left allocated. */
 int moe_ctx_create(const moe_config_t* cfg, const moe_weights_t* w, moe_ctx_t** out);
@@ -262,7 +265,9 @@ int moe_dispatch_layout(moe_ctx_t* ctx, int phase, hipStream_t stream);
 int moe_dispatch_permute(moe_ctx_t* ctx, int phase, const void* x, hipStream_t stream);
 
 /* Grouped expert FFN (DISPATCHED -> COMPUTED): h = silu(x_perm W1^T) *
- * (x_perm W3^T) and y = h W2^T for the rows of every resident expert.  bf16
+ * (x_perm W3^T) and y = h W2^T for the rows of every resident expert: the
+ * expert computation between DeepEP's dispatch and combine (Section 2.2; the
+ * experts of the evaluated model, Section 7.1, in BF16 or FP8).  bf16
  * contexts multiply bf16 operands with float32 accumulation, round h to bf16
  * (nearest even; h is GEMM2's operand) and keep y in float32; float32
  * contexts compute everything in float32.  The tile schedule
@@ -276,13 +281,17 @@ int moe_expert_ffn(moe_ctx_t* ctx, int phase, hipStream_t stream);
 
 /* Weighted combine (COMPUTED -> IDLE): out[t] = sum over resident slots j, in
  * slot order, of topk_w[t,j] * y[row_of_slot[t,j]], accumulated in float32;
- * tokens with no resident slot get a zero row.
+ * tokens with no resident slot get a zero row.  The receive side of DeepEP's
+ * combine (Section 2.2) on this GPU's share of the experts: summing the
+ * shares of all expert-parallel ranks gives the layer's output.
  * out: borrowed device [T, H] float32; every row is written.
  * Errors: MOE_ERR_INVALID_ARG (null out with T > 0), MOE_ERR_INVALID_PHASE,
  * MOE_ERR_STATE, MOE_ERR_HIP. */
 int moe_combine(moe_ctx_t* ctx, int phase, void* out, hipStream_t stream);
 
-/* Fill *view with the phase's buffer pointers and state.
+/* Fill *view with the phase's buffer pointers and state: the phase-owned
+ * objects of Section 5.1, read-only for the caller (parity checks, and the
+ * stable addresses a captured D graph replays against, Section 6.1).
  * Errors: MOE_ERR_INVALID_ARG (null), MOE_ERR_INVALID_PHASE. */
 int moe_phase_view(const moe_ctx_t* ctx, int phase, moe_phase_view_t* view);
 

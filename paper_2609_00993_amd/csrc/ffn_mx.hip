@@ -137,7 +137,7 @@ struct GemmArgsMX {
   const int32_t* tile_base;
   long long b_stride, bs_stride;
   int e_loc, N, K, n_tiles, up_row;
-  int n_group, xcd_local;
+  int n_group, m_super, xcd_local;
   YieldTo yield;
 };
 

@@ -31,8 +31,9 @@ __device__ __forceinline__ void dense_tile_at(const G& g, int L, int bm, int bn,
 }
 
 // Coordinates of logical tile L.  Tiles run expert-major.  Within an expert
-// (mt m-tiles x n_tiles n-tiles) the n-tiles are cut into blocks of n_group;
-// block by block, the tiles go m-tile by m-tile, n-tile fastest.  So
+// (mt m-tiles x n_tiles n-tiles), optionally cut into super-rows of m_super
+// m-tiles taken one after another, the n-tiles are cut into blocks of
+// n_group; block by block, the tiles go m-tile by m-tile, n-tile fastest.  So
 // consecutive tiles (which one XCD runs side by side, see block_tile) share
 // an activation row block across n_group n-tiles and a weight n-tile across
 // the m-tiles running together.  n_group = n_tiles is plain m-major order.
@@ -70,16 +71,27 @@ __device__ __forceinline__ void tile_at(const G& g, int L, int bm, int bn, TileC
     mt = j - q * mt_e;
     nt = 8 * q + (local & 7);
   } else {
+    // Super-rows (m_super > 0): the expert's m-tiles are cut into runs of
+    // m_super, each run taking all its n-tiles before the next (the last run
+    // may be shorter); within a run the n-block order below applies.
+    int m_base = 0, sm = mt_e, r0 = local;
+    if (g.m_super > 0) {
+      const int run = g.m_super * g.n_tiles;
+      const int sr = local / run;
+      m_base = sr * g.m_super;
+      sm = min(g.m_super, mt_e - m_base);
+      r0 = local - sr * run;
+    }
     const int b = g.n_group;
     const int full = g.n_tiles / b;  // full n-blocks; a narrower one may follow
-    int blk = local / (mt_e * b), bw = b;
+    int blk = r0 / (sm * b), bw = b;
     if (blk >= full) {
       blk = full;
       bw = g.n_tiles - full * b;
     }
-    const int r = local - blk * mt_e * b;
-    mt = r / bw;
-    nt = blk * b + (r - mt * bw);
+    const int r = r0 - blk * sm * b;
+    mt = m_base + r / bw;
+    nt = blk * b + (r - (r / bw) * bw);
   }
   const int beg = g.offsets[e], rows = g.offsets[e + 1] - beg;
   const int per = (g.xcd_local == 1 || g.xcd_local == 2) ? (rows + mt_e - 1) / mt_e : bm;

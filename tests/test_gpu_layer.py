@@ -63,6 +63,10 @@ SPECS = {
                                                   T_P=2100, T_D=3), seed=16),
     "wide-k128-bf16": lambda: make_layer(LayerSpec("wide-k128-bf16", E=4, e0=0, E_loc=4, k=1, H=128, I=192,
                                                    dtype=BF16, T_P=2100, T_D=3), seed=17),
+    # GEMM1's 256-row tiles in super-rows: 32 n-tiles (the last one partial)
+    # give super-rows of 8 m-tiles, over experts of nine or ten m-tiles
+    "wide-super-bf16": lambda: make_layer(LayerSpec("wide-super-bf16", E=2, e0=0, E_loc=2, k=1, H=64, I=4032,
+                                                    dtype=BF16, T_P=4700, T_D=3), seed=18),
     # k = E: every expert takes every token
     "k-eq-E-bf16": lambda: make_layer(LayerSpec("kE-bf16", E=4, e0=0, E_loc=4, k=4, H=64, I=64, dtype=BF16, T_P=129,
                                                 T_D=1), seed=14),

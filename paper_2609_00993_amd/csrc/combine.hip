@@ -11,16 +11,22 @@
 // 16-byte vectors of y from exactly the resident rows (row ids and weights
 // are read back as wave-uniform values), so y is read once per row and out
 // written once per token, fully coalesced, with no per-element slot loads.
-// Up to four resident rows are loaded before they are added, in slot order.
+// Several resident rows are loaded before they are added, in slot order.
 #include "common.h"
 #include "kernels.h"
 
 namespace moepd {
 
-constexpr int kCombVec = 4;  // 16-byte vectors per lane per pass
+// Large batches: four 16-byte vectors per lane per pass, four resident rows
+// loaded together.  Small batches (up to 2048 tokens, split over more waves
+// per row): two and two, which holds the kernel to 35 registers per lane, so
+// its waves fit on a CU beside the other phase's large GEMM tiles (the
+// 256-row bf16 tiles leave 56 per SIMD lane) instead of waiting for one of
+// those tiles to finish (config 3, D's combine under P: 100 -> 41 us).
+constexpr int kCombVec = 4, kCombGroup = 4;
+constexpr int kCombVecSmall = 2, kCombGroupSmall = 2;
 
-constexpr int kCombGroup = 4;  // resident rows loaded together
-
+template <int VEC, int GROUP>
 __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ y, const float* __restrict__ topk_w,
                                                       const int32_t* __restrict__ row_of_slot, int T, int k, int nv,
                                                       int parts, u32x4* __restrict__ out, WindowSignal close) {
@@ -35,20 +41,20 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ 
   const float w_l = lane < k ? topk_w[(size_t)t * k + lane] : 0.f;
   const uint64_t resident = __ballot(r_l >= 0);
   u32x4* o = out + (size_t)t * nv;
-  constexpr int PASS = kWave * kCombVec;
+  constexpr int PASS = kWave * VEC;
   for (int v0 = part * PASS; v0 < nv; v0 += parts * PASS) {
-    float acc[kCombVec][4];
+    float acc[VEC][4];
 #pragma unroll
-    for (int i = 0; i < kCombVec; ++i)
+    for (int i = 0; i < VEC; ++i)
 #pragma unroll
       for (int e = 0; e < 4; ++e) acc[i][e] = 0.f;
     uint64_t m = resident;
-    while (m) {  // resident slots in ascending slot order, up to kCombGroup at a time
-      int r[kCombGroup];
-      float w[kCombGroup];
+    while (m) {  // resident slots in ascending slot order, up to GROUP at a time
+      int r[GROUP];
+      float w[GROUP];
       int n = 0;
 #pragma unroll
-      for (int q = 0; q < kCombGroup; ++q) {
+      for (int q = 0; q < GROUP; ++q) {
         r[q] = 0;
         w[q] = 0.f;
         if (m) {
@@ -59,28 +65,28 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ 
           n = q + 1;
         }
       }
-      u32x4 a[kCombGroup][kCombVec];
+      u32x4 a[GROUP][VEC];
 #pragma unroll
-      for (int q = 0; q < kCombGroup; ++q) {
+      for (int q = 0; q < GROUP; ++q) {
         if (q < n) {
           const u32x4* yr = y + (size_t)r[q] * nv;
 #pragma unroll
-          for (int i = 0; i < kCombVec; ++i) {
+          for (int i = 0; i < VEC; ++i) {
             const int v = v0 + i * kWave + lane;
             if (v < nv) a[q][i] = yr[v];
           }
         }
       }
 #pragma unroll
-      for (int q = 0; q < kCombGroup; ++q)
+      for (int q = 0; q < GROUP; ++q)
         if (q < n)
 #pragma unroll
-          for (int i = 0; i < kCombVec; ++i)
+          for (int i = 0; i < VEC; ++i)
 #pragma unroll
             for (int e = 0; e < 4; ++e) acc[i][e] += w[q] * __uint_as_float(a[q][i][e]);
     }
 #pragma unroll
-    for (int i = 0; i < kCombVec; ++i) {
+    for (int i = 0; i < VEC; ++i) {
       const int v = v0 + i * kWave + lane;
       if (v < nv) {
         u32x4 q;
@@ -96,10 +102,15 @@ hipError_t launch_combine(const void* y, const float* topk_w, const int32_t* row
                           void* out, WindowSignal close, hipStream_t s) {
   if (T <= 0) return hipSuccess;
   const int nv = H * 4 / 16;
-  const int parts = waves_per_row(T, nv, kCombVec);
+  const bool small = T <= 2048;
+  const int parts = waves_per_row(T, nv, small ? kCombVecSmall : kCombVec);
   const long long waves = (long long)T * parts;
-  combine_kernel<<<dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s>>>(
-      (const u32x4*)y, topk_w, row_of_slot, T, k, nv, parts, (u32x4*)out, close);
+  if (small)
+    combine_kernel<kCombVecSmall, kCombGroupSmall><<<dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s>>>(
+        (const u32x4*)y, topk_w, row_of_slot, T, k, nv, parts, (u32x4*)out, close);
+  else
+    combine_kernel<kCombVec, kCombGroup><<<dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s>>>(
+        (const u32x4*)y, topk_w, row_of_slot, T, k, nv, parts, (u32x4*)out, close);
   return hipGetLastError();
 }
 

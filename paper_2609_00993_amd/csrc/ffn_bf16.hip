@@ -687,7 +687,7 @@ static inline int round8(long long v) { return (int)((v + 7) / 8 * 8); }
 
 hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
                            int e_loc, int H, int I, int max_m_tiles, bool stage, YieldTo yield, hipStream_t s) {
-  GemmArgs g;
+  GemmArgs g{};
   g.yield = yield;
   g.offsets = b.offsets;
   g.tile_base = b.tile_base;

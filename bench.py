@@ -67,7 +67,8 @@ def parse():
                          "is the headline, 4 the agentic trace on the config-2 layer, 5 the config-2 layer in MX FP8, "
                          "6/7 the paper's model shape in FP8/BF16")
     ap.add_argument("--trace-steps", type=int, default=200, help="steps of the agentic trace (config 4)")
-    ap.add_argument("--d-iters", type=int, default=60, help="D layers per latency measurement")
+    ap.add_argument("--d-iters", type=int, default=200,
+                    help="D layers per latency measurement (enough to span some twenty P layers under P)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="least time of the CPU-oracle sample")
     ap.add_argument("--cpu-tokens", type=int, default=4096, help="P tokens in the CPU-oracle sample (at most)")
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -1,6 +1,7 @@
 // Tile scheduling shared by the grouped GEMMs (bf16 and MX FP8): logical
 // tile ids, their (expert, row block, column block) coordinates, and the
-// XCD-aware mapping of workgroups to tiles.  G is a GEMM argument struct
+// XCD-aware mapping of workgroups to tiles.  The mapping itself is plain
+// arithmetic, compiled for the host too, where a test checks it.  G is a GEMM argument struct
 // with offsets, tile_base, e_loc, n_tiles, n_group and xcd_local (and the
 // dense_* fields for the dense mode).
 #pragma once
@@ -19,7 +20,7 @@ struct TileCoord {
 // Tile of a dense GEMM: splits outermost, then m-tiles, n-tile fastest (the
 // n-tiles of one row block run side by side and share its activation rows).
 template <class G>
-__device__ __forceinline__ void dense_tile_at(const G& g, int L, int bm, int bn, TileCoord& tc) {
+__host__ __device__ __forceinline__ void dense_tile_at(const G& g, int L, int bm, int bn, TileCoord& tc) {
   const int per_split = g.dense_total / g.dense_splits;
   const int s = L / per_split, r = L - s * per_split;
   const int mt = r / g.n_tiles;
@@ -54,7 +55,7 @@ __device__ __forceinline__ void dense_tile_at(const G& g, int L, int bm, int bn,
 // few weight bytes) and another many rare ones (few m-tiles each, many
 // bytes); the tile counts match but the bytes to fetch do not.
 template <class G>
-__device__ __forceinline__ void tile_at(const G& g, int L, int bm, int bn, TileCoord& tc) {
+__host__ __device__ __forceinline__ void tile_at(const G& g, int L, int bm, int bn, TileCoord& tc) {
   int lo = 0, hi = g.e_loc - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
@@ -121,23 +122,29 @@ __device__ __forceinline__ void tile_at(const G& g, int L, int bm, int bn, TileC
 // every XCD takes a share of it.
 constexpr int kXcdGroup = 32;  // workgroups one XCD runs at a time: one per CU
 
+// Logical tile of the workgroup with block id b (see block_tile).
 template <bool DENSE = false, class G>
-__device__ __forceinline__ int block_tile(const G& g) {
+__host__ __device__ __forceinline__ int tile_of_block(const G& g, int b) {
   int total;
   if constexpr (DENSE) total = g.dense_total;
   else total = g.tile_base[g.e_loc] * g.n_tiles;
   if (g.xcd_local == 3) {
-    const int x = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int x = b & 7, slot = b >> 3;
     const int base = slot / kXcdGroup * (8 * kXcdGroup), j = slot % kXcdGroup;
     const int L = base + 8 * kXcdGroup <= total ? base + x * kXcdGroup + j : base + 8 * j + x;
     return L < total ? L : -1;
   }
-  if (g.xcd_local != 1) return (int)blockIdx.x < total ? (int)blockIdx.x : -1;
+  if (g.xcd_local != 1) return b < total ? b : -1;
   const int per_xcd = (total + 7) >> 3;
-  const int slot = blockIdx.x >> 3;
+  const int slot = b >> 3;
   if (slot >= per_xcd) return -1;
-  const int L = (blockIdx.x & 7) * per_xcd + slot;
+  const int L = (b & 7) * per_xcd + slot;
   return L < total ? L : -1;
+}
+
+template <bool DENSE = false, class G>
+__device__ __forceinline__ int block_tile(const G& g) {
+  return tile_of_block<DENSE>(g, (int)blockIdx.x);
 }
 
 // D first (Section 3.1): the planner admits ready D work before P, and a

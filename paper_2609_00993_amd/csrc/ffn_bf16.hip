@@ -302,10 +302,11 @@ __device__ __forceinline__ void gemm_skinny(const GemmArgs& g) {
 // The pipeline has three levels:
 //  * DMA: once every wave has read slice kt out of its slot (the barrier at
 //    the end of slice kt), slice kt + STAGES is issued into that slot, so
-//    STAGES - 1 slices are in flight while one is multiplied.  Only this
+//    STAGES - 1 slices are in flight while one is multiplied.  The group goes
+//    out in parts over the next slice's substeps (see PART_N).  Only this
 //    wave's DMA instructions (and older stores) count in vmcnt, and loads
 //    complete in order, so wait_vmcnt(n * per-slice count) retires exactly
-//    the slices needed;
+//    the slices needed: every group is issued whole before the next begins;
 //  * fragments: each 16-deep substep's A/B fragments are read from LDS into
 //    one of two register sets while the MFMAs of the previous substep run on
 //    the other (the read of a slice's first substep crosses the barrier);
@@ -377,6 +378,15 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   static_assert(STAGES >= 2 && NPS * (STAGES - 1) < 64, "pipeline depth");
   constexpr int LEAD = SA - STAGES;  // slices the activations run ahead of the weights
   static_assert(LEAD == 0 || (LEAD == 1 && STAGES == 2 && !WIN && !DENSE), "activation lead: two weight slots only");
+  // The DMA group a slice end issues goes out in SUB parts: the first at the
+  // slice end, the others one per substep of the next slice (into the slot
+  // the barrier freed), so the vector-memory queue takes a part at a time
+  // beside the MFMAs instead of the whole group at once.  Without the lead
+  // all of the group's NPS instructions are cut into parts; with it, the
+  // weights (one slice to land) go out whole at the slice end and only the
+  // activations' A_INS are.
+  constexpr int PART_N = LEAD == 1 ? A_INS : NPS;
+  constexpr int PART0 = PART_N / SUB;  // instructions of part 0
   static_assert(2 * A_INS + B_INS < 64, "prologue wait range");
   // One LDS object: the activation and weight rings of K slices, then (WIN)
   // the cells of the D window word (its first word in each cell, see
@@ -429,23 +439,37 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
       b_src[i] = Be + (size_t)brow * g.K + k0 + (lphys ^ swz<BK>(r)) * 8;
     }
   };
+  auto issue_a1 = [&](int i, int koff, int slot) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, MOEPD_LPTR(&lds.a[slot][(wave * A_INS + i) * 64]), 16,
+                                             a_off[i] + (uint32_t)koff * 2u, 0, 0, 0);
+  };
+  auto issue_b1 = [&](int i, int koff, int slot) {
+    __builtin_amdgcn_global_load_lds(MOEPD_GPTR(b_src[i] + koff), MOEPD_LPTR(&lds.b[slot][(wave * B_INS + i) * 64]), 16,
+                                     0, 0);
+  };
   auto issue_a = [&](int kt, int slot) {
-    const int koff = kt * BK;
 #pragma unroll
-    for (int i = 0; i < A_INS; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, MOEPD_LPTR(&lds.a[slot][(wave * A_INS + i) * 64]), 16,
-                                               a_off[i] + (uint32_t)koff * 2u, 0, 0, 0);
+    for (int i = 0; i < A_INS; ++i) issue_a1(i, kt * BK, slot);
   };
   auto issue_b = [&](int kt, int slot) {
-    const int koff = kt * BK;
 #pragma unroll
-    for (int i = 0; i < B_INS; ++i)
-      __builtin_amdgcn_global_load_lds(MOEPD_GPTR(b_src[i] + koff), MOEPD_LPTR(&lds.b[slot][(wave * B_INS + i) * 64]),
-                                       16, 0, 0);
+    for (int i = 0; i < B_INS; ++i) issue_b1(i, kt * BK, slot);
   };
-  // DMA group of slice j: without a lead, A(j) then B(j) into slot j % STAGES;
-  // with the activation lead, B(j) into weight slot j % 2, then A(j + 1) (if
-  // the tile has it) into activation slot (j + 1) % 3.
+  // Part p of slice kt's spread DMA into slot `slot`: instructions
+  // [PART_N p / SUB, PART_N (p + 1) / SUB) of A's A_INS then B's B_INS
+  // (with the lead, of A's alone).  p is a constant once the loops around a
+  // call are unrolled, and so is every branch here.
+  auto issue_part = [&](int kt, int slot, int p) {
+#pragma unroll
+    for (int i = PART_N * p / SUB; i < PART_N * (p + 1) / SUB; ++i) {
+      if (LEAD == 1 || i < A_INS) issue_a1(i, kt * BK, slot);
+      else issue_b1(i - A_INS, kt * BK, slot);
+    }
+  };
+  // DMA group of slice j, whole (the prologue's): without a lead, A(j) then
+  // B(j) into slot j % STAGES; with the activation lead, B(j) into weight
+  // slot j % 2, then A(j + 1) (if the tile has it) into activation slot
+  // (j + 1) % 3.
   auto issue = [&](int kt, int bslot, int aslot_next) {
     if constexpr (LEAD == 0) {
       issue_a(kt, bslot);
@@ -537,15 +561,29 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   // the barrier; MODE 1: no slices left to issue; MODE 2: the tile's last
   // slice (no barrier, nothing to read ahead).  The three loops below keep
   // each body straight-line code, so the accumulators stay in place.
-  auto slice = [&](auto mode, int kt, int aslot, int bslot) {
+  // PEND: the group the previous slice end started is still going out; its
+  // parts 1 .. SUB - 1 are issued here, one per substep, into the slot that
+  // the previous slice freed: the group of slice kt - 1 + STAGES, or with the
+  // lead A(kt + 2) (whose weights went out whole with part 0).
+  auto slice = [&](auto mode, auto pend, int kt, int aslot, int bslot) {
     constexpr int MODE = decltype(mode)::value;
+    constexpr bool PEND = decltype(pend)::value;
+    int pkt, pslot;
+    if constexpr (LEAD == 1) {
+      pkt = kt + 2;
+      pslot = aslot + 2 >= SA ? aslot + 2 - SA : aslot + 2;
+    } else {
+      pkt = kt - 1 + STAGES;
+      pslot = bslot == 0 ? STAGES - 1 : bslot - 1;
+    }
 #pragma unroll
     for (int sub = 0; sub < SUB; ++sub) {
       const int cur = sub & 1, nxt = cur ^ 1;
       if (sub + 1 < SUB) {
         read_frags(aslot, bslot, sub + 1, fa[nxt], fb[nxt]);
+        if constexpr (PEND) issue_part(pkt, pslot, sub + 1);
         mfmas(fa[cur], fb[cur]);
-        interleave<0, NMF, 0, NRD, 0>();
+        interleave<0, NMF, PEND ? (PART_N + SUB - 1) / SUB : 0, NRD, 0>();
       } else if constexpr (MODE < 2) {
         // Every read of this slot is in registers once lgkmcnt is 0.  Slice
         // kt + 1 has landed once at most min(STAGES - 2, KT - 2 - kt) newer
@@ -566,7 +604,16 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
         if (nb == STAGES) nb = 0;
         if (na == SA) na = 0;
         if constexpr (MODE == 0) {
-          issue(kt + STAGES, bslot, aslot);
+          if constexpr (LEAD == 1) {
+            // Branch-free, so the scheduler can spread the group between the
+            // MFMAs: at the last MODE-0 slice (kt + 3 = KT) the part reloads
+            // from slice KT - 1 into this slot, which no later slice of the
+            // tile reads (they read slots (KT - 2) % 3 and (KT - 1) % 3).
+            issue_b(kt + STAGES, bslot);
+            issue_part(min(kt + STAGES + 1, KT - 1), aslot, 0);
+          } else {
+            issue_part(kt + STAGES, bslot, 0);
+          }
           // D first inside a tile: every kPauseEvery slices, a P tile that
           // found the D window open at the previous check (or at the tile's
           // start) pauses until it closes (within the tile's wait budget), so
@@ -584,7 +631,7 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
         }
         read_frags(na, nb, 0, fa[nxt], fb[nxt]);
         mfmas(fa[cur], fb[cur]);
-        interleave<0, NMF, MODE == 0 ? NPS : 0, NRD, 1>();
+        interleave<0, NMF, MODE == 0 ? (LEAD == 1 ? B_INS : 0) + PART0 : 0, NRD, 1>();
       } else {
         mfmas(fa[cur], fb[cur]);
       }
@@ -595,15 +642,32 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
     if (++bslot == STAGES) bslot = 0;
     if (++aslot == SA) aslot = 0;
   };
-  for (; kt < KT - STAGES; ++kt) {
-    slice(std::integral_constant<int, 0>{}, kt, aslot, bslot);
+  using M0 = std::integral_constant<int, 0>;
+  using M1 = std::integral_constant<int, 1>;
+  using NoPend = std::false_type;
+  using Pend = std::true_type;
+  if (KT > STAGES) {
+    // the prologue issued its groups whole: nothing pending in slice 0
+    slice(M0{}, NoPend{}, kt, aslot, bslot);
     advance();
+    for (++kt; kt < KT - STAGES; ++kt) {
+      slice(M0{}, Pend{}, kt, aslot, bslot);
+      advance();
+    }
+    // Without the lead, the group of slice KT - 1 (started at the last MODE-0
+    // slice end) still goes out in the first MODE-1 slice; with it, only a
+    // reload nothing reads was started there, and nothing is pending.
+    if constexpr (LEAD == 0) {
+      slice(M1{}, Pend{}, kt, aslot, bslot);
+      advance();
+      ++kt;
+    }
   }
   for (; kt < KT - 1; ++kt) {
-    slice(std::integral_constant<int, 1>{}, kt, aslot, bslot);
+    slice(M1{}, NoPend{}, kt, aslot, bslot);
     advance();
   }
-  slice(std::integral_constant<int, 2>{}, kt, aslot, bslot);
+  slice(std::integral_constant<int, 2>{}, NoPend{}, kt, aslot, bslot);
 
   // epilogue: SwiGLU -> bf16 h (four columns = one 8-byte store), or
   // float32 y (four columns = one 16-byte store).  A lane's row is fixed,

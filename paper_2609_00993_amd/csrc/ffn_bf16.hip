@@ -378,15 +378,18 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   static_assert(STAGES >= 2 && NPS * (STAGES - 1) < 64, "pipeline depth");
   constexpr int LEAD = SA - STAGES;  // slices the activations run ahead of the weights
   static_assert(LEAD == 0 || (LEAD == 1 && STAGES == 2 && !WIN && !DENSE), "activation lead: two weight slots only");
-  // The DMA group a slice end issues goes out in SUB parts: the first at the
-  // slice end, the others one per substep of the next slice (into the slot
-  // the barrier freed), so the vector-memory queue takes a part at a time
-  // beside the MFMAs instead of the whole group at once.  Without the lead
-  // all of the group's NPS instructions are cut into parts; with it, the
-  // weights (one slice to land) go out whole at the slice end and only the
-  // activations' A_INS are.
-  constexpr int PART_N = LEAD == 1 ? A_INS : NPS;
-  constexpr int PART0 = PART_N / SUB;  // instructions of part 0
+  // The DMA group a slice end would issue goes out in parts, so the
+  // vector-memory queue takes a part at a time beside the MFMAs instead of
+  // the whole group at once.  Without the lead the group's NPS instructions
+  // make SUB parts: the first at the slice end, the others one per substep
+  // of the next slice (into the slot the barrier freed).  With it the
+  // weights (one slice to land) go out whole at the slice end and the
+  // activations' A_INS make SUB - 1 parts, one per substep of the next slice
+  // but its last (their slot too was freed a barrier earlier).
+  constexpr int PART_N = LEAD == 1 ? A_INS : NPS;       // instructions cut into parts
+  constexpr int NPART = LEAD == 1 ? SUB - 1 : SUB;      // parts
+  constexpr int END_PARTS = NPART - (SUB - 1);         // parts issued at the slice end (0 or 1)
+  constexpr int PART0 = END_PARTS * PART_N / NPART;     // instructions among them
   static_assert(2 * A_INS + B_INS < 64, "prologue wait range");
   // One LDS object: the activation and weight rings of K slices, then (WIN)
   // the cells of the D window word (its first word in each cell, see
@@ -456,12 +459,12 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
     for (int i = 0; i < B_INS; ++i) issue_b1(i, kt * BK, slot);
   };
   // Part p of slice kt's spread DMA into slot `slot`: instructions
-  // [PART_N p / SUB, PART_N (p + 1) / SUB) of A's A_INS then B's B_INS
+  // [PART_N p / NPART, PART_N (p + 1) / NPART) of A's A_INS then B's B_INS
   // (with the lead, of A's alone).  p is a constant once the loops around a
   // call are unrolled, and so is every branch here.
   auto issue_part = [&](int kt, int slot, int p) {
 #pragma unroll
-    for (int i = PART_N * p / SUB; i < PART_N * (p + 1) / SUB; ++i) {
+    for (int i = PART_N * p / NPART; i < PART_N * (p + 1) / NPART; ++i) {
       if (LEAD == 1 || i < A_INS) issue_a1(i, kt * BK, slot);
       else issue_b1(i - A_INS, kt * BK, slot);
     }
@@ -561,10 +564,10 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   // the barrier; MODE 1: no slices left to issue; MODE 2: the tile's last
   // slice (no barrier, nothing to read ahead).  The three loops below keep
   // each body straight-line code, so the accumulators stay in place.
-  // PEND: the group the previous slice end started is still going out; its
-  // parts 1 .. SUB - 1 are issued here, one per substep, into the slot that
-  // the previous slice freed: the group of slice kt - 1 + STAGES, or with the
-  // lead A(kt + 2) (whose weights went out whole with part 0).
+  // PEND: a group is still going out, one part per substep, into the slot
+  // that the previous slice freed: parts 1 .. SUB - 1 of the group of slice
+  // kt - 1 + STAGES (its part 0 went out at the previous slice end), or with
+  // the lead all SUB - 1 parts of A(kt + 2) (B(kt + 1) went out whole there).
   auto slice = [&](auto mode, auto pend, int kt, int aslot, int bslot) {
     constexpr int MODE = decltype(mode)::value;
     constexpr bool PEND = decltype(pend)::value;
@@ -581,9 +584,9 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
       const int cur = sub & 1, nxt = cur ^ 1;
       if (sub + 1 < SUB) {
         read_frags(aslot, bslot, sub + 1, fa[nxt], fb[nxt]);
-        if constexpr (PEND) issue_part(pkt, pslot, sub + 1);
+        if constexpr (PEND) issue_part(pkt, pslot, END_PARTS + sub);
         mfmas(fa[cur], fb[cur]);
-        interleave<0, NMF, PEND ? (PART_N + SUB - 1) / SUB : 0, NRD, 0>();
+        interleave<0, NMF, PEND ? (PART_N + NPART - 1) / NPART : 0, NRD, 0>();
       } else if constexpr (MODE < 2) {
         // Every read of this slot is in registers once lgkmcnt is 0.  Slice
         // kt + 1 has landed once at most min(STAGES - 2, KT - 2 - kt) newer
@@ -604,16 +607,8 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
         if (nb == STAGES) nb = 0;
         if (na == SA) na = 0;
         if constexpr (MODE == 0) {
-          if constexpr (LEAD == 1) {
-            // Branch-free, so the scheduler can spread the group between the
-            // MFMAs: at the last MODE-0 slice (kt + 3 = KT) the part reloads
-            // from slice KT - 1 into this slot, which no later slice of the
-            // tile reads (they read slots (KT - 2) % 3 and (KT - 1) % 3).
-            issue_b(kt + STAGES, bslot);
-            issue_part(min(kt + STAGES + 1, KT - 1), aslot, 0);
-          } else {
-            issue_part(kt + STAGES, bslot, 0);
-          }
+          if constexpr (LEAD == 1) issue_b(kt + STAGES, bslot);
+          else issue_part(kt + STAGES, bslot, 0);
           // D first inside a tile: every kPauseEvery slices, a P tile that
           // found the D window open at the previous check (or at the tile's
           // start) pauses until it closes (within the tile's wait budget), so
@@ -631,7 +626,7 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
         }
         read_frags(na, nb, 0, fa[nxt], fb[nxt]);
         mfmas(fa[cur], fb[cur]);
-        interleave<0, NMF, MODE == 0 ? (LEAD == 1 ? B_INS : 0) + PART0 : 0, NRD, 1>();
+        interleave<0, NMF, MODE == 0 ? (LEAD == 1 ? B_INS : PART0) : 0, NRD, 1>();
       } else {
         mfmas(fa[cur], fb[cur]);
       }
@@ -655,8 +650,8 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
       advance();
     }
     // Without the lead, the group of slice KT - 1 (started at the last MODE-0
-    // slice end) still goes out in the first MODE-1 slice; with it, only a
-    // reload nothing reads was started there, and nothing is pending.
+    // slice end) still goes out in the first MODE-1 slice; with it, the last
+    // MODE-0 slice end issued B(KT - 1) alone, and nothing is pending.
     if constexpr (LEAD == 0) {
       slice(M1{}, Pend{}, kt, aslot, bslot);
       advance();

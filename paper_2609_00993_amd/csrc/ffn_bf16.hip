@@ -664,6 +664,56 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
   }
   slice(std::integral_constant<int, 2>{}, NoPend{}, kt, aslot, bslot);
 
+  // float32 y goes out through LDS (the ring is free once every wave has
+  // read its last slice): each 32 x 32 block is written to the wave's own
+  // LDS area in the accumulator layout, one 128-byte row per block row with
+  // its 16-byte chunks XOR-swizzled by the row, and read back row-major, so
+  // each store instruction writes eight whole 128-byte lines of y instead of
+  // 32-byte pieces of 32 rows.  A block's 32 columns are all in range or all
+  // out (N is a multiple of 64); rows past the expert's end are not stored.
+  // Within a wave LDS operations complete in order, so a block's read-back
+  // sees its writes and the next round's writes follow this round's reads.
+  constexpr int NBLK = FM * FN;                                   // 32 x 32 blocks per wave
+  constexpr int STAGE_BLK = sizeof(lds) / (4 * 4096);            // blocks one wave can stage
+  constexpr int EPI_BLK = NBLK < STAGE_BLK ? NBLK : STAGE_BLK;   // per round (the last may hold fewer)
+  constexpr bool STAGED_Y = !GATED && !DENSE && EPI_BLK > 0;
+  if constexpr (STAGED_Y) {
+    // every wave's reads of the ring are in registers (lgkmcnt 0; vmcnt is
+    // already 0 after the last slice) before any wave overwrites it
+    wait_vmcnt_lgkm0<63>();
+    bare_barrier();
+    u32x4* stage = reinterpret_cast<u32x4*>(&lds) + wave * (EPI_BLK * 256);
+    const int wr = lane & 31, wh = lane >> 5;  // accumulator row, column half
+    const int rr0 = lane >> 3, rc = lane & 7;  // read-back row (of 8), chunk
+#pragma unroll
+    for (int b0 = 0; b0 < NBLK; b0 += EPI_BLK) {
+#pragma unroll
+      for (int bi = 0; bi < EPI_BLK && b0 + bi < NBLK; ++bi) {
+        const int fm = (b0 + bi) / FN, fn = (b0 + bi) % FN;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x4 v = {acc[fm][fn][4 * q], acc[fm][fn][4 * q + 1], acc[fm][fn][4 * q + 2],
+                           acc[fm][fn][4 * q + 3]};
+          stage[bi * 256 + wr * 8 + ((2 * q + wh) ^ (wr & 7))] = __builtin_bit_cast(u32x4, v);
+        }
+      }
+#pragma unroll
+      for (int bi = 0; bi < EPI_BLK && b0 + bi < NBLK; ++bi) {
+        const int fm = (b0 + bi) / FN, fn = (b0 + bi) % FN;
+        const int col0 = tc.n0 + wn * WTN + fn * 32;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const int rr = 8 * p + rr0;
+          const u32x4 v = stage[bi * 256 + rr * 8 + (rc ^ (rr & 7))];
+          const int row = tc.m0 + wm * WTM + fm * 32 + rr;
+          if (row < tc.m_end && col0 < g.N)
+            *reinterpret_cast<u32x4*>(static_cast<float*>(g.C) + (size_t)row * g.N + col0 + 4 * rc) = v;
+        }
+      }
+    }
+    return;
+  }
+
   // epilogue: SwiGLU -> bf16 h (four columns = one 8-byte store), or
   // float32 y (four columns = one 16-byte store).  A lane's row is fixed,
   // so it is checked once per 32-row block.  N is a multiple of 64, so a

@@ -767,17 +767,16 @@ __global__ __launch_bounds__(256) void gemm2_down_prefill(GemmArgs g) { gemm_rin
 // so that small batches still spread over the GPU.
 __global__ __launch_bounds__(256) void router_gemm(GemmArgs g) { gemm_ring_body<64, 128, 64, 2, 2, false, 3, true>(g); }
 // The wide tiles never yield (a P workgroup waiting on its CU would only keep
-// D off it), so they leave out the window cells.  GEMM1's take 64-deep
+// D off it), so they leave out the window cells.  Both GEMMs take 64-deep
 // slices, two weight slots and three activation slots, the activations one
-// slice ahead (160 KB; at the 16384-token skewed batch 4 % faster than
-// 32-deep slices in four stages, and the third activation slot 1.4 % faster
-// than a two-slot ring); GEMM2 measured the same either way and keeps the
-// four-stage ring of 32-deep slices.
+// slice ahead and their DMA spread over the next slice's substeps (160 KB).
+// At the 16384-token skewed batch that ring is 4 % faster than 32-deep slices
+// in four stages for GEMM1, and 8 % for GEMM2 once the DMA is spread.
 __global__ __launch_bounds__(256) void gemm1_swiglu_wide(GemmArgs g) {
   gemm_ring_body<256, 256, 64, 2, 2, true, 2, false, 3, false>(g);
 }
 __global__ __launch_bounds__(256) void gemm2_down_wide(GemmArgs g) {
-  gemm_ring_body<256, 256, 32, 2, 2, false, 4, false, 4, false>(g);
+  gemm_ring_body<256, 256, 64, 2, 2, false, 2, false, 3, false>(g);
 }
 template <bool ROT, bool STAGE>
 __global__ __launch_bounds__(64 * kDecodeWaves) void gemm1_swiglu_decode(GemmArgs g) {

@@ -453,7 +453,12 @@ int moe_expert_ffn(moe_ctx_t* ctx, int phase, hipStream_t stream) {
     const long long rows = (long long)p.T * kk;
     const int max_m_tiles = (int)((rows + p.bm - 1) / p.bm) + c.num_local_experts;
     ctx->ffn_regime[phase].store(p.regime, std::memory_order_relaxed);
-    const bool stage = ctx->ffn_regime[phase ^ 1].load(std::memory_order_relaxed) != 0;
+    const int other = ctx->ffn_regime[phase ^ 1].load(std::memory_order_relaxed);
+    const bool stage = other != 0;
+    // D first (Section 3.1) on one GPU: while D-first admission is on and the
+    // context runs D layers, P's 256-row GEMM2 takes the tile that leaves a CU
+    // room for D's decode tiles beside it.
+    const bool share = phase == MOE_PHASE_P && c.d_priority_us > 0 && other != -1;
     for (int gemm = 1; gemm <= 2; ++gemm) {
       st = timed(p, gemm == 1 ? MOE_KERNEL_GEMM1 : MOE_KERNEL_GEMM2, stream, [&] {
         if (c.dtype == MOE_DTYPE_FP8)
@@ -462,7 +467,7 @@ int moe_expert_ffn(moe_ctx_t* ctx, int phase, hipStream_t stream) {
                                c.num_local_experts, c.hidden, c.inter, max_m_tiles, yield_of(ctx, phase), stream);
         if (c.dtype == MOE_DTYPE_BF16)
           return launch_ffn_bf16(p.regime, gemm, p.b, ctx->w.w_gate_up, ctx->w.w_down, c.num_local_experts, c.hidden,
-                                 c.inter, max_m_tiles, stage, yield_of(ctx, phase), stream);
+                                 c.inter, max_m_tiles, stage, share, yield_of(ctx, phase), stream);
         return launch_ffn_f32(gemm, p.b, ctx->w.w_gate_up, ctx->w.w_down, c.num_local_experts, c.hidden, c.inter,
                               max_m_tiles, stream);
       });

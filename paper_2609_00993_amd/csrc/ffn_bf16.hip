@@ -767,16 +767,24 @@ __global__ __launch_bounds__(256) void gemm2_down_prefill(GemmArgs g) { gemm_rin
 // so that small batches still spread over the GPU.
 __global__ __launch_bounds__(256) void router_gemm(GemmArgs g) { gemm_ring_body<64, 128, 64, 2, 2, false, 3, true>(g); }
 // The wide tiles never yield (a P workgroup waiting on its CU would only keep
-// D off it), so they leave out the window cells.  Both GEMMs take 64-deep
-// slices, two weight slots and three activation slots, the activations one
-// slice ahead and their DMA spread over the next slice's substeps (160 KB).
-// At the 16384-token skewed batch that ring is 4 % faster than 32-deep slices
-// in four stages for GEMM1, and 8 % for GEMM2 once the DMA is spread.
+// D off it), so they leave out the window cells.  They take two weight slots
+// and three activation slots, the activations one slice ahead and their DMA
+// spread over the next slice's substeps, in 64-deep slices (160 KB; at the
+// 16384-token skewed batch 4 % faster than 32-deep slices in four stages for
+// GEMM1, 8 % for GEMM2).  GEMM2's share form takes 32-deep slices (80 KB,
+// 364 registers), which leaves a CU room for D's staged GEMM2 tiles beside
+// it: at that batch D's layer under P took 985 us against 1360-1400 us
+// beside the 64-deep form (460 registers) and 1085 us beside a four-stage
+// ring of 32-deep slices (128 KB).  Nothing of D's GEMM1 fits beside GEMM1's
+// tile in either depth (456-460 registers).
 __global__ __launch_bounds__(256) void gemm1_swiglu_wide(GemmArgs g) {
   gemm_ring_body<256, 256, 64, 2, 2, true, 2, false, 3, false>(g);
 }
 __global__ __launch_bounds__(256) void gemm2_down_wide(GemmArgs g) {
   gemm_ring_body<256, 256, 64, 2, 2, false, 2, false, 3, false>(g);
+}
+__global__ __launch_bounds__(256) void gemm2_down_wide_share(GemmArgs g) {
+  gemm_ring_body<256, 256, 32, 2, 2, false, 2, false, 3, false>(g);
 }
 template <bool ROT, bool STAGE>
 __global__ __launch_bounds__(64 * kDecodeWaves) void gemm1_swiglu_decode(GemmArgs g) {
@@ -794,7 +802,8 @@ int ffn_bf16_bm(int regime) { return regime == 0 ? 160 : regime == 2 ? 256 : 32;
 static inline int round8(long long v) { return (int)((v + 7) / 8 * 8); }
 
 hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
-                           int e_loc, int H, int I, int max_m_tiles, bool stage, YieldTo yield, hipStream_t s) {
+                           int e_loc, int H, int I, int max_m_tiles, bool stage, bool share, YieldTo yield,
+                           hipStream_t s) {
   GemmArgs g{};
   g.yield = yield;
   g.offsets = b.offsets;
@@ -846,6 +855,7 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
       else gemm2_down_prefill<<<grid, 256, 0, s>>>(g);
     } else {
       if (gemm == 1) gemm1_swiglu_wide<<<grid, 256, 0, s>>>(g);
+      else if (share) gemm2_down_wide_share<<<grid, 256, 0, s>>>(g);
       else gemm2_down_wide<<<grid, 256, 0, s>>>(g);
     }
   } else {

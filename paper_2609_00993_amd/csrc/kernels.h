@@ -142,9 +142,13 @@ hipError_t launch_combine(const void* y, const float* topk_w, const int32_t* row
 int ffn_bf16_bm(int regime);
 // stage (decode regime only): load operands as whole lines through a per-wave
 // LDS stage (faster), or straight into registers with no LDS, so the tiles fit
-// on CUs held by the other phase's 160-row prefill tiles.
+// on CUs held by the other phase's 160-row prefill tiles.  share (256-row
+// regime, GEMM2 only): take the tile that leaves each CU room for the other
+// phase's staged decode GEMM2 tiles (80 KB of LDS and 364 registers instead
+// of 160 KB and 460; the same bits, 12 % slower alone).
 hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
-                           int e_loc, int H, int I, int max_m_tiles, bool stage, YieldTo yield, hipStream_t s);
+                           int e_loc, int H, int I, int max_m_tiles, bool stage, bool share, YieldTo yield,
+                           hipStream_t s);
 
 // MX FP8 contexts: the phase's x_perm and h regions hold E4M3 codes
 // followed by their E8M0 scale bytes (one per 32 values of a row).

@@ -144,6 +144,30 @@ def test_concurrent_phases_bit_identical_to_solo(d_priority_us):
         g.close()
 
 
+@pytest.mark.parametrize("name", ["wide-bf16", "wide-k64-bf16", "wide-super-bf16"])
+def test_wide_gemm2_share_form(name):
+    """P's 256-row GEMM2 takes its share form (32-deep slices, room for D's
+    decode tiles on each CU) once D-first admission is on and the context has
+    run a D layer.  Both forms add the K products in the same order, so P
+    gives the same bits before D's first layer (64-deep form) and after it
+    (share form), and both pass the oracle checks."""
+    inp = SPECS[name]()
+    g = GpuLayer(inp, d_priority_us=500)
+    try:
+        g.run(0)  # no D layer yet: the 64-deep form
+        first = _snapshot(g, 0)
+        check_phase(g, inp, 0)
+        g.run(1)
+        g.run(0)  # the share form
+        second = _snapshot(g, 0)
+        for key in first:
+            assert np.array_equal(first[key], second[key]), key
+        check_phase(g, inp, 0)
+        check_phase(g, inp, 1)
+    finally:
+        g.close()
+
+
 def test_abandoned_d_window_is_not_honoured():
     """A D layer abandoned after its route leaves its window open on the
     device; after moe_phase_reset the P phase no longer waits for it (the

@@ -167,7 +167,7 @@ struct MxWeights {
 // x (bf16 rows) -> MX FP8 codes and scales of every resident row.
 hipError_t launch_permute_mx(const void* x, int T, int k, int H, const int32_t* row_of_slot, uint8_t* codes,
                              uint8_t* scales, hipStream_t s);
-// regime 0: large batches (128-row LDS-ring tiles); 1: small batches
+// regime 0: large batches (256-row LDS-ring tiles); 1: small batches
 // (32-row weight-streaming tiles).
 int ffn_mx_bm(int regime);
 hipError_t launch_ffn_mx(int regime, int gemm, const PhaseBuffers& b, const MxBuffers& mx, const MxWeights& w,

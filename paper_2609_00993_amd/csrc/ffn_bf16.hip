@@ -350,12 +350,13 @@ constexpr int kCachePolicyAgent = 0x10;  // sc1: coherent at agent scope
 
 // STAGES slots hold weight slices; SA >= STAGES slots hold activation
 // slices.  With SA = STAGES + 1 (two weight slots only) the activation
-// slices are issued one slice further ahead than the weight slices: slice j's
-// DMA group is [B(j), A(j + 1)], so the counted wait at a slice end retires
-// the next slice's weights while that slice's activations, issued a slice
-// earlier, have had two slices' time to land.  WIN: the tile keeps the LDS
-// cells of the D window word (tiles that never yield leave them out, which
-// frees the LDS for the third activation slot).
+// slices run one slice further ahead than the weight slices: the slice end
+// that issues B(j) is followed, over the next slice's substeps, by A(j + 1),
+// so the counted wait at a slice end retires the next slice's weights while
+// that slice's activations, issued a slice earlier, have had up to two
+// slices' time to land.  WIN: the tile keeps the LDS cells of the D window
+// word (tiles that never yield leave them out, which frees the LDS for the
+// third activation slot).
 template <int BM, int BR, int BK, int WM, int WN, bool GATED, int STAGES, bool DENSE = false, int SA = STAGES,
           bool WIN = true>
 __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {

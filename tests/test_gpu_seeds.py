@@ -17,7 +17,9 @@ Each draw picks:
 - an even or skewed router bias.
 
 Expert row counts, ragged tails, empty experts and experts off this GPU
-therefore vary from seed to seed.
+therefore vary from seed to seed.  Odd seeds run D's layer first with
+D-first admission on, so P takes the tiles it uses beside D (the share form
+of the 256-row GEMM2).
 
 The checks are the fixed shapes' own: exact routing and layout, then every
 stage within the dtype's bound (h and y element by element for bf16 and
@@ -144,11 +146,14 @@ def check_dense(g, inp, ph):
 @pytest.mark.parametrize("seed", list(SEEDS))
 def test_seeded_layer_parity(seed, need_gpu):
     spec, bias = draw(seed)
-    print(f"[seed {seed}] {spec} bias={'skewed' if bias is not None else 'none'}", flush=True)
+    # odd seeds: D first with D-first admission on, so P's 256-row GEMM2 takes
+    # its share form and P's 160-row tiles carry the D window word
+    d_first = seed % 2 == 1
+    print(f"[seed {seed}] {spec} bias={'skewed' if bias is not None else 'none'} d_first={d_first}", flush=True)
     inp = make_layer(spec, seed=500 + seed, bias=bias)
-    g = GpuLayer(inp)
+    g = GpuLayer(inp, d_priority_us=500 if d_first else 0)
     try:
-        for ph in (0, 1):
+        for ph in ((1, 0) if d_first else (0, 1)):
             g.run(ph)
         check = check_fp8 if spec.dtype == FP8 else check_dense
         for ph in (0, 1):

@@ -149,8 +149,11 @@ typedef struct moe_config {
    * start of its moe_route kernel to the start of its moe_combine kernel), a P
    * grouped-GEMM workgroup about to start a tile, or at every fourth K slice
    * of a running tile, waits for the D layer, for at most about this many
-   * microseconds per tile in all.  A scheduling hint only: results are
-   * unchanged. */
+   * microseconds per tile in all.  P's tiles of very large batches (256 rows,
+   * at least 512 rows per expert expected) never wait, since each holds a
+   * whole CU; once the context has run a D layer, their GEMM2 takes a form
+   * that leaves each CU room for D's tiles instead.  A scheduling hint only:
+   * results are unchanged. */
   int32_t d_priority_us;
 } moe_config_t;
 

@@ -409,6 +409,7 @@ def run_trace(args, M, inp, dev):
             "note": "per-step D layer latency; alone = the same D steps with no P batches",
         },
         "roofline": roof,
+        "roofline_phase_alone": roof_alone,
         "kernels": kernels,
         "kernels_pass_note": "per-kernel HIP events over a replay of the trace with D-first admission off",
         "without_d_first": {
@@ -760,6 +761,25 @@ def main():
                 kern[(ph, M.moe_kernel_name(kid))] = (ms, n)
     M.check(M.moe_timing_enable(ctx_off, 0))
 
+    # ---- the same kernels with each phase alone (K layers back to back on
+    # its stream, per-kernel events).  In the concurrent steps the D stream's
+    # K layers run beside the first few P layers, and while D's waves hold a
+    # CU a P tile that needs the whole CU cannot start there, so those P
+    # launches take longer; the launches of a phase alone show what the
+    # kernel itself reaches.
+    kern_alone = {}
+    M.check(M.moe_timing_enable(ctx_off, args.steps), "moe_timing_enable")
+    for ph in (0, 1):
+        for _ in range(args.steps):
+            layer(ph, ctx_off)
+        torch.cuda.synchronize()
+        for kid in range(M.MOE_NUM_KERNELS):
+            st, ms, n = M.moe_timing_read(ctx_off, ph, kid)
+            M.check(st)
+            if n:
+                kern_alone[(ph, M.moe_kernel_name(kid))] = (ms, n)
+    M.check(M.moe_timing_enable(ctx_off, 0))
+
     # rows and touched experts of each phase (device-side layout, read once)
     rows, touched, t_res = {}, {}, {}
     for ph in (0, 1):
@@ -895,6 +915,16 @@ def main():
     roof["traffic"] = recorded_traffic(args.config, ph_d, name_d)
     roof["kernel"] = f"{name_d} ({'P' if ph_d == 0 else 'D'})"
     roof["per_launch"] = {"bytes": by, "flops": fl, "mean_us": round(avg_s * 1e6, 2), "launches": n_d}
+    roof_alone = None
+    if dom in kern_alone:
+        ms_a, n_a = kern_alone[dom]
+        avg_a = ms_a / n_a / 1e3
+        ach_a = (fl / avg_a / 1e12) if roof["unit"] == "TFLOP/s" else (by / avg_a / 1e9)
+        roof_alone = {"achieved": round(ach_a, 2), "frac": round(ach_a / roof["peak"], 4), "unit": roof["unit"],
+                      "mean_us": round(avg_a * 1e6, 2), "launches": n_a,
+                      "note": "the same kernel and units, its phase's layers alone back to back (per-kernel "
+                              "events); the roofline above averages the concurrent steps, where the other phase "
+                              "holds some of the CUs during the first few layers"}
 
     kernels = {}
     for (ph, name), (ms, n) in sorted(kern.items()):
@@ -939,6 +969,7 @@ def main():
                     "(P streams the same weights)",
         },
         "roofline": roof,
+        "roofline_phase_alone": roof_alone,
         "engine_clock_mhz": clock,
         "segments": segments,
         "router_from_hidden": router,

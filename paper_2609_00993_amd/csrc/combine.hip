@@ -17,16 +17,20 @@
 
 namespace moepd {
 
-// Large batches: four 16-byte vectors per lane per pass, four resident rows
-// loaded together.  Small batches (up to 2048 tokens, split over more waves
-// per row): two and two, which holds the kernel to 35 registers per lane, so
-// its waves fit on a CU beside the other phase's large GEMM tiles (the
-// 256-row bf16 tiles leave 56 per SIMD lane) instead of waiting for one of
-// those tiles to finish (config 3, D's combine under P: 100 -> 41 us).
-constexpr int kCombVec = 4, kCombGroup = 4;
+// Large batches: four 16-byte vectors per lane per pass, and up to eight
+// resident rows (all of a top-8 token's) loaded together, so a pass waits
+// for memory once; y is read with nontemporal loads, since each row is read
+// once and y (2.8 GB at the 16384-token skewed batch) is far larger than
+// the caches.  At that batch the combine went 667 -> 607 us alone.  Small
+// batches (up to 2048 tokens, split over more waves per row): two vectors
+// and two rows, plain loads, which holds the kernel to 35 registers per
+// lane, so its waves fit on a CU beside the other phase's large GEMM tiles
+// (the 256-row bf16 tiles leave 52 per SIMD lane) instead of waiting for
+// one of those tiles to finish (config 3, D's combine under P: 100 -> 41 us).
+constexpr int kCombVec = 4, kCombGroup = 8;
 constexpr int kCombVecSmall = 2, kCombGroupSmall = 2;
 
-template <int VEC, int GROUP>
+template <int VEC, int GROUP, bool STREAM>
 __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ y, const float* __restrict__ topk_w,
                                                       const int32_t* __restrict__ row_of_slot, int T, int k, int nv,
                                                       int parts, u32x4* __restrict__ out, WindowSignal close) {
@@ -73,7 +77,10 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ 
 #pragma unroll
           for (int i = 0; i < VEC; ++i) {
             const int v = v0 + i * kWave + lane;
-            if (v < nv) a[q][i] = yr[v];
+            if (v < nv) {
+              if constexpr (STREAM) a[q][i] = __builtin_nontemporal_load(&yr[v]);
+              else a[q][i] = yr[v];
+            }
           }
         }
       }
@@ -106,10 +113,10 @@ hipError_t launch_combine(const void* y, const float* topk_w, const int32_t* row
   const int parts = waves_per_row(T, nv, small ? kCombVecSmall : kCombVec);
   const long long waves = (long long)T * parts;
   if (small)
-    combine_kernel<kCombVecSmall, kCombGroupSmall><<<dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s>>>(
+    combine_kernel<kCombVecSmall, kCombGroupSmall, false><<<dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s>>>(
         (const u32x4*)y, topk_w, row_of_slot, T, k, nv, parts, (u32x4*)out, close);
   else
-    combine_kernel<kCombVec, kCombGroup><<<dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s>>>(
+    combine_kernel<kCombVec, kCombGroup, true><<<dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s>>>(
         (const u32x4*)y, topk_w, row_of_slot, T, k, nv, parts, (u32x4*)out, close);
   return hipGetLastError();
 }

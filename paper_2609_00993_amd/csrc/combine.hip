@@ -19,11 +19,13 @@ namespace moepd {
 
 // Large batches: four 16-byte vectors per lane per pass, and up to eight
 // resident rows (all of a top-8 token's) loaded together, so a pass waits
-// for memory once; y is read with nontemporal loads, since each row is read
-// once and y (2.8 GB at the 16384-token skewed batch) is far larger than
-// the caches.  At that batch the combine went 667 -> 607 us alone.  Small
+// for memory once.  y is read and out written with nontemporal accesses:
+// each row of y is read once, y (2.8 GB at the 16384-token skewed batch) is
+// far larger than the caches, and out lines left dirty in them would be
+// written back while the next layer's dispatch runs.  At that batch the
+// combine and the next permute went 667 + 297 -> 614 + 295 us alone.  Small
 // batches (up to 2048 tokens, split over more waves per row): two vectors
-// and two rows, plain loads, which holds the kernel to 35 registers per
+// and two rows, plain accesses, which holds the kernel to 35 registers per
 // lane, so its waves fit on a CU beside the other phase's large GEMM tiles
 // (the 256-row bf16 tiles leave 52 per SIMD lane) instead of waiting for
 // one of those tiles to finish (config 3, D's combine under P: 100 -> 41 us).
@@ -99,7 +101,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ 
         u32x4 q;
 #pragma unroll
         for (int e = 0; e < 4; ++e) q[e] = __float_as_uint(acc[i][e]);
-        o[v] = q;
+        if constexpr (STREAM) __builtin_nontemporal_store(q, &o[v]);
+        else o[v] = q;
       }
     }
   }

@@ -237,7 +237,7 @@ WindowSignal window_of(moe_ctx* ctx, int phase) {
 // The P phase's grouped GEMMs hold back while the D window is open; one poll
 // sleeps 127 * 64 cycles, about 3.4 us at 2.4 GHz.  Not for tiles whose
 // workgroups hold too many registers for a D GEMM wave to share their SIMDs
-// (the bf16 256-row tiles, 460 VGPRs; the MX FP8 ring tiles, 320): a P
+// (the bf16 256-row tiles, 460 VGPRs; the MX FP8 ring tiles, 476-480): a P
 // workgroup waiting on its CU would only keep D off it.
 YieldTo yield_of(moe_ctx* ctx, int phase) {
   if (phase != MOE_PHASE_P || ctx->cfg.d_priority_us <= 0) return YieldTo{nullptr, 0, 0};

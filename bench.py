@@ -409,7 +409,6 @@ def run_trace(args, M, inp, dev):
             "note": "per-step D layer latency; alone = the same D steps with no P batches",
         },
         "roofline": roof,
-        "roofline_phase_alone": roof_alone,
         "kernels": kernels,
         "kernels_pass_note": "per-kernel HIP events over a replay of the trace with D-first admission off",
         "without_d_first": {

@@ -656,7 +656,7 @@ def solo_run(args, M, c, ph, layer, spec, T, esz, osz):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build runs the path on a single "
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the library runs the layer on a single "
               f"MI355X and has no multi-GPU step.", file=sys.stderr)
         sys.exit(2)
 

@@ -21,6 +21,8 @@ JSON line with:
   steps (the events themselves cost stream time, so the throughput pass runs
   without them) with D-first admission off, so that a P kernel's duration is
   its own work and not the waits the admission policy puts in it;
+  roofline_phase_alone: the same kernel timed over K layers of its phase
+  alone, with no layer of the other phase beside it;
 * D-first admission (--d-priority-us, default 500): while a D layer is in
   flight, P grouped-GEMM tiles wait for it (at tile starts and every few K
   slices), up to that bound per tile; value and d_latency_us are measured

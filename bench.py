@@ -129,18 +129,26 @@ def kernel_units(spec, kernel, T, R, touched, esz, osz=None, t_res=None):
     return 0, 0
 
 
-def recorded_traffic(cfg, phase, kernel):
+def recorded_traffic(cfg, phase, kernel, lib_path=None):
     """HBM bytes per launch of one kernel from the committed rocprofv3 counter
     record (FETCH_SIZE + WRITE_SIZE, each scaled by a plain copy's reading),
-    or None when no record exists or a kernel source changed since."""
+    or None when no record exists or the kernels differ from the profiled
+    ones: the record holds for the library file it was taken with (lib_path,
+    the library this process loaded) and for the kernel sources it was taken
+    on."""
     import hashlib
+
+    def sha(p):
+        return hashlib.sha256(open(p, "rb").read()).hexdigest()
 
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     try:
         rec = json.load(open(path))
-        for rel, digest in rec["sources"].items():
-            if hashlib.sha256(open(os.path.join(ROOT, rel), "rb").read()).hexdigest() != digest:
-                return None
+        same_lib = bool(lib_path) and os.path.exists(lib_path) and rec.get("library_sha256") == sha(lib_path)
+        if not same_lib:
+            for rel, digest in rec["sources"].items():
+                if sha(os.path.join(ROOT, rel)) != digest:
+                    return None
         return rec["workloads"][f"cfg{cfg}"][f"{'P' if phase == 0 else 'D'}.{kernel}"]["hbm_bytes"]
     except (OSError, KeyError, ValueError):
         return None
@@ -913,7 +921,7 @@ def main():
         achieved = by / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = round(achieved / roof["peak"], 4)
-    roof["traffic"] = recorded_traffic(args.config, ph_d, name_d)
+    roof["traffic"] = recorded_traffic(args.config, ph_d, name_d, M.LIB_PATH)
     roof["kernel"] = f"{name_d} ({'P' if ph_d == 0 else 'D'})"
     roof["per_launch"] = {"bytes": by, "flops": fl, "mean_us": round(avg_s * 1e6, 2), "launches": n_d}
     roof_alone = None

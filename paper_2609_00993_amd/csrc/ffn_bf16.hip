@@ -16,7 +16,13 @@
 // (the dispatcher deals workgroups round-robin to the 8 XCDs): the m-tiles of
 // one expert that share a weight tile run side by side on one XCD's L2.
 //
-// Two tile shapes:
+// Three tile shapes, picked by the expected rows per expert:
+//  * very large batches (at least 512 rows per expert): 256 x (128 gate +
+//    128 up) or 256 x 256 tiles, a 2 x 2 grid of waves, 64-deep K slices in
+//    two weight slots and three activation slots (160 KB), the activations
+//    one slice ahead; GEMM2 also has a share form in 32-deep slices that
+//    leaves a CU room for the other phase's decode tiles (gemm_ring_body and
+//    the kernels below);
 //  * large batches (prefill): 256 threads, 160 x (128 gate + 128 up) or
 //    160 x 256 output tiles, 32x32x16 MFMAs, the four waves side by side
 //    along N.  Operands stream HBM -> LDS with global_load_lds_dwordx4 into a

@@ -145,6 +145,7 @@ int alloc_phase(moe_ctx* ctx, int phase) {
   // The signal slot is 16 bytes: the grouped GEMMs read the window word in it
   // with a 16-byte LDS DMA (its other words stay zero).
   const size_t o_cc = take((size_t)E * mc * 4), o_tb = take((E + 1) * 4), o_sig = take(16);
+  const size_t o_td = take(c.dtype == MOE_DTYPE_BF16 ? (size_t)ffn_bf16_handover_words(p.rows_cap, E, c.hidden) * 4 : 0);
 
   void* mem = nullptr;
   if (hipMalloc(&mem, off) != hipSuccess || !mem) {
@@ -165,10 +166,11 @@ int alloc_phase(moe_ctx* ctx, int phase) {
   p.b.chunk_counts = (int32_t*)(base + o_cc);
   p.b.tile_base = (int32_t*)(base + o_tb);
   p.b.signal = (int32_t*)(base + o_sig);
+  p.b.tile_done = (int32_t*)(base + o_td);
   p.b.logits = (float*)(base + o_lg);
   p.b.partials = (float*)(base + o_part);
-  // Zero the small metadata (counts, offsets, tile prefix, signal word) once
-  // at creation.
+  // Zero the small metadata (counts, offsets, tile prefix, signal word, tile
+  // marks) once at creation.
   if (hipMemset(base + o_cnt, 0, o_ros - o_cnt) != hipSuccess) return MOE_ERR_HIP;
   if (hipMemset(base + o_tb, 0, off - o_tb) != hipSuccess) return MOE_ERR_HIP;
   if (hipEventCreateWithFlags(&p.ev, hipEventDisableTiming) != hipSuccess) {
@@ -467,7 +469,8 @@ int moe_expert_ffn(moe_ctx_t* ctx, int phase, hipStream_t stream) {
                                c.num_local_experts, c.hidden, c.inter, max_m_tiles, yield_of(ctx, phase), stream);
         if (c.dtype == MOE_DTYPE_BF16)
           return launch_ffn_bf16(p.regime, gemm, p.b, ctx->w.w_gate_up, ctx->w.w_down, c.num_local_experts, c.hidden,
-                                 c.inter, max_m_tiles, stage, share, yield_of(ctx, phase), stream);
+                                 c.inter, max_m_tiles, stage, share, yield_of(ctx, phase),
+                                 ctx->ph[phase ^ 1].b.signal, stream);
         return launch_ffn_f32(gemm, p.b, ctx->w.w_gate_up, ctx->w.w_down, c.num_local_experts, c.hidden, c.inter,
                               max_m_tiles, stream);
       });

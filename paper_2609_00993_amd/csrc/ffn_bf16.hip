@@ -70,6 +70,12 @@ struct GemmArgs {
   // partial product to C + s * dense_rows * N.  dense_total = m-tiles x
   // n-tiles x splits.
   int dense_rows, dense_splits, dense_ks, dense_total;
+  // Hand-over pair of the 256-row GEMM2 (see launch_ffn_bf16): 0 = off;
+  // 1 = full tiles, a tile that starts while *window is nonzero is left to
+  // the second launch; 2 = share tiles, a tile marked done is skipped.
+  int handoff;
+  const int32_t* window;
+  int32_t* tile_done;
 };
 
 // First 64-deep K block of a decode tile (of nk blocks).  When a row of K
@@ -536,6 +542,30 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
 
   const int L = block_tile<DENSE>(g);
   if (L < 0) return;
+  // Hand-over pair: one thread decides for the workgroup (whether the other
+  // phase has a layer in flight now, or whether the first launch did this
+  // tile) and passes the decision through the ring's first LDS word, which no
+  // DMA has touched yet, so every wave leaves or stays together.
+  constexpr bool HANDOFF = !GATED && !DENSE && BM == 256;
+  if constexpr (HANDOFF) {
+    if (g.handoff) {
+      int* cell = reinterpret_cast<int*>(&lds);
+      if (threadIdx.x == 0) {
+        int skip;
+        if (g.handoff == 1) {
+          skip = __hip_atomic_load(g.window, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+        } else {
+          skip = g.tile_done[L];
+          if (skip) g.tile_done[L] = 0;
+        }
+        *cell = skip;
+      }
+      __syncthreads();
+      const int skip = *cell;
+      __syncthreads();  // every wave has read the word before the ring's DMA lands
+      if (skip) return;
+    }
+  }
   int wait_budget = g.yield.polls;  // shared by the tile's start and in-tile waits
   yield_to_window(g.yield, wait_budget);
   TileCoord tc;
@@ -718,6 +748,9 @@ __device__ __forceinline__ void gemm_ring_body(const GemmArgs& g) {
         }
       }
     }
+    if constexpr (HANDOFF) {
+      if (g.handoff == 1 && threadIdx.x == 0) g.tile_done[L] = 1;
+    }
     return;
   }
 
@@ -808,9 +841,13 @@ int ffn_bf16_bm(int regime) { return regime == 0 ? 160 : regime == 2 ? 256 : 32;
 
 static inline int round8(long long v) { return (int)((v + 7) / 8 * 8); }
 
+long long ffn_bf16_handover_words(long long rows_cap, int e_loc, int H) {
+  return (rows_cap / 256 + 1 + e_loc) * (long long)((H + 255) / 256);
+}
+
 hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
                            int e_loc, int H, int I, int max_m_tiles, bool stage, bool share, YieldTo yield,
-                           hipStream_t s) {
+                           const int32_t* other_window, hipStream_t s) {
   GemmArgs g{};
   g.yield = yield;
   g.offsets = b.offsets;
@@ -861,9 +898,23 @@ hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const vo
       if (gemm == 1) gemm1_swiglu_prefill<<<grid, 256, 0, s>>>(g);
       else gemm2_down_prefill<<<grid, 256, 0, s>>>(g);
     } else {
-      if (gemm == 1) gemm1_swiglu_wide<<<grid, 256, 0, s>>>(g);
-      else if (share) gemm2_down_wide_share<<<grid, 256, 0, s>>>(g);
-      else gemm2_down_wide<<<grid, 256, 0, s>>>(g);
+      if (gemm == 1) {
+        gemm1_swiglu_wide<<<grid, 256, 0, s>>>(g);
+      } else if (share && other_window) {
+        // the full tiles while the other phase is idle, then the share form
+        // for the tiles they left (the second launch follows the first on
+        // the stream, so it sees every mark)
+        g.window = other_window;
+        g.tile_done = b.tile_done;
+        g.handoff = 1;
+        gemm2_down_wide<<<grid, 256, 0, s>>>(g);
+        g.handoff = 2;
+        gemm2_down_wide_share<<<grid, 256, 0, s>>>(g);
+      } else if (share) {
+        gemm2_down_wide_share<<<grid, 256, 0, s>>>(g);
+      } else {
+        gemm2_down_wide<<<grid, 256, 0, s>>>(g);
+      }
     }
   } else {
     constexpr int bn = 32 * kDecodeWaves, threads = 64 * kDecodeWaves;

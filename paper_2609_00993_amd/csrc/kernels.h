@@ -27,6 +27,10 @@ struct PhaseBuffers {
   // by this phase's kernels; read by the other phase's grouped GEMMs.  It is
   // the first word of a zeroed 16-byte slot (read as one 16-byte vector).
   int32_t* signal;
+  // One word per tile of the 256-row GEMM2 run as a hand-over pair (see
+  // launch_ffn_bf16): 1 = done by the first launch, cleared by the second.
+  // Zero between layers.
+  int32_t* tile_done;
   // router GEMM (moe_route_from_hidden)
   float* logits;    // [Tmax, E] float32, the logits top-k selects from
   float* partials;  // [router_cap_rows, E] float32, K-split partial products
@@ -143,12 +147,18 @@ int ffn_bf16_bm(int regime);
 // stage (decode regime only): load operands as whole lines through a per-wave
 // LDS stage (faster), or straight into registers with no LDS, so the tiles fit
 // on CUs held by the other phase's 160-row prefill tiles.  share (256-row
-// regime, GEMM2 only): take the tile that leaves each CU room for the other
+// regime, GEMM2 only): the tiles that leave each CU room for the other
 // phase's staged decode GEMM2 tiles (80 KB of LDS and 364 registers instead
-// of 160 KB and 460; the same bits, 12 % slower alone).
+// of 160 KB and 460; the same bits, 12 % slower alone) run only while the
+// other phase has a layer in flight: a first launch of the full tiles does
+// every tile that starts while `other_window` (the other phase's signal word)
+// is 0 and marks it in b.tile_done, and a second launch of the share form
+// does the rest.
 hipError_t launch_ffn_bf16(int regime, int gemm, const PhaseBuffers& b, const void* w_gu, const void* w_dn,
                            int e_loc, int H, int I, int max_m_tiles, bool stage, bool share, YieldTo yield,
-                           hipStream_t s);
+                           const int32_t* other_window, hipStream_t s);
+// Words of b.tile_done a phase needs (256-row GEMM2 tiles at its capacity).
+long long ffn_bf16_handover_words(long long rows_cap, int e_loc, int H);
 
 // MX FP8 contexts: the phase's x_perm and h regions hold E4M3 codes
 // followed by their E8M0 scale bytes (one per 32 values of a row).

@@ -168,6 +168,57 @@ def test_wide_gemm2_share_form(name):
         g.close()
 
 
+def _poison_y(g, ph):
+    """Fill the phase's y with NaN bits, so a tile no kernel wrote shows."""
+    import ctypes
+
+    import torch
+
+    from tests.gpu_util import hip
+
+    torch.cuda.synchronize()
+    st, v = g.M.moe_phase_view(g.ctx, ph)
+    g.M.check(st)
+    h = hip()
+    h.hipMemset.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t]
+    h.hipMemset.restype = ctypes.c_int
+    assert h.hipMemset(v.y, 0xFF, v.rows_capacity * g.spec.H * 4) == 0
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("name", ["wide-bf16", "wide-k64-bf16"])
+def test_wide_gemm2_handover(name):
+    """With D-first admission on and a D layer run, P's 256-row GEMM2 is a
+    hand-over pair: a launch of the full tiles does every tile that starts
+    while D has no layer in flight, and a launch of the share form does the
+    rest.  With D idle the first launch does them all; with D's window held
+    open (D's route enqueued, the rest of its layer not) the second does.
+    y is poisoned before each P layer, so a tile that neither launch did
+    would show; every run gives the bits of the full form alone."""
+    inp = SPECS[name]()
+    g = GpuLayer(inp, d_priority_us=500)
+    M = g.M
+    try:
+        g.run(0)  # no D layer yet: the full form alone
+        ref = _snapshot(g, 0)
+        g.run(1)
+        for held in (False, True, False):
+            if held:
+                M.check(M.moe_route(g.ctx, 1, g.logits[1], g.T[1], g.streams[1]))
+            _poison_y(g, 0)
+            g.run(0)
+            got = _snapshot(g, 0)
+            for key in ref:
+                assert np.array_equal(ref[key], got[key]), (held, key)
+            if held:
+                M.check(M.moe_phase_reset(g.ctx, 1))
+                g.run(1)  # a whole D layer closes the window again
+        check_phase(g, inp, 0)
+        check_phase(g, inp, 1)
+    finally:
+        g.close()
+
+
 def test_abandoned_d_window_is_not_honoured():
     """A D layer abandoned after its route leaves its window open on the
     device; after moe_phase_reset the P phase no longer waits for it (the

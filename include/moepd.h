@@ -151,9 +151,9 @@ typedef struct moe_config {
    * of a running tile, waits for the D layer, for at most about this many
    * microseconds per tile in all.  P's tiles of very large batches (256 rows,
    * at least 512 rows per expert expected) never wait, since each holds a
-   * whole CU; once the context has run a D layer, their GEMM2 takes a form
-   * that leaves each CU room for D's tiles instead.  A scheduling hint only:
-   * results are unchanged. */
+   * whole CU; once the context has run a D layer, a GEMM2 tile that starts
+   * while a D layer is in flight takes a form that leaves its CU room for
+   * D's tiles instead.  A scheduling hint only: results are unchanged. */
   int32_t d_priority_us;
 } moe_config_t;
 

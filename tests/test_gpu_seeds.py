@@ -18,8 +18,8 @@ Each draw picks:
 
 Expert row counts, ragged tails, empty experts and experts off this GPU
 therefore vary from seed to seed.  Odd seeds run D's layer first with
-D-first admission on, so P takes the tiles it uses beside D (the share form
-of the 256-row GEMM2).
+D-first admission on, so P takes the tiles it uses beside D (the 256-row
+GEMM2 as a hand-over pair of the full and the share form).
 
 The checks are the fixed shapes' own: exact routing and layout, then every
 stage within the dtype's bound (h and y element by element for bf16 and
@@ -146,8 +146,8 @@ def check_dense(g, inp, ph):
 @pytest.mark.parametrize("seed", list(SEEDS))
 def test_seeded_layer_parity(seed, need_gpu):
     spec, bias = draw(seed)
-    # odd seeds: D first with D-first admission on, so P's 256-row GEMM2 takes
-    # its share form and P's 160-row tiles carry the D window word
+    # odd seeds: D first with D-first admission on, so P's 256-row GEMM2 runs
+    # as the hand-over pair and P's 160-row tiles carry the D window word
     d_first = seed % 2 == 1
     print(f"[seed {seed}] {spec} bias={'skewed' if bias is not None else 'none'} d_first={d_first}", flush=True)
     inp = make_layer(spec, seed=500 + seed, bias=bias)
